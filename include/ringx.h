@@ -1,0 +1,131 @@
+/*
+ * ringx.h -- C ABI of libringx: ring-chunked, non-causal multi-head attention on one MI355X
+ * (gfx950), i.e. one GPU's share of RingX sequence parallelism (arXiv 2507.16697, Sec. III-A).
+ *
+ * One query shard attends to the full key/value sequence, which arrives as R ring-step chunks.
+ * Each chunk yields a partial output loc_out_r and log-sum-exp loc_lse_r (Sec. III-A, text after
+ * Eq. (5)); the partials are merged exactly by Eq. (5).  The backward recomputes the softmax from
+ * the merged log-sum-exp.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  Layout     Tensors are contiguous [B, H, N, d] (d fastest), the scaled_dot_product_attention
+ *             convention (Sec. VI calls RingX a drop-in for it).  lse and part_lse are fp32
+ *             [.., B, H, Nq], natural logarithm of sum_j exp(scale * q_i . k_j).
+ *  Semantics  Non-causal, no mask, no dropout.  Scores are scale * q . k (scale is an explicit
+ *             argument; the paper's Eqs. (1)/(4) print no scale).
+ *  dtype      RINGX_BF16: q, k, v, out, dout are bf16; products on bf16 MFMA with fp32
+ *             accumulation; softmax statistics, merge, lse and gradients in fp32.
+ *             RINGX_FP32: every tensor fp32, fp32 arithmetic throughout.
+ *  Chunks     Chunk r of R covers keys [floor(r*Nk/R), floor((r+1)*Nk/R)); 1 <= R <= Nk.
+ *  Memory     Every tensor pointer is caller-owned device memory, 16-byte aligned; outputs must
+ *             not overlap inputs.  The library never allocates, frees or keeps a pointer after
+ *             returning.  Scratch memory needed by the backward is passed in by the caller.
+ *  Ordering   Work is enqueued on `stream` (0 = the null stream) and the call returns without
+ *             synchronising.  There is no global mutable state; calls are thread-safe.
+ *  Errors     Arguments are checked on the host before any HIP call.  On an error status nothing
+ *             has been enqueued and no output has been written.  RINGX_E_HIP reports a launch
+ *             failure (hipGetLastError) after validation passed; outputs are then undefined.
+ *             No C++ exception crosses the ABI.
+ */
+#ifndef RINGX_H
+#define RINGX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__HIPCC__) || defined(__HIP_PLATFORM_AMD__)
+#include <hip/hip_runtime_api.h>
+#else
+typedef struct ihipStream_t* hipStream_t;
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum ringx_status {
+  RINGX_OK = 0,
+  RINGX_E_NULLPTR = 1,     /* a required pointer is NULL                                     */
+  RINGX_E_SHAPE = 2,       /* B, H, Nq, Nk < 1, a size overflows, or scale not finite and > 0 */
+  RINGX_E_CHUNKS = 3,      /* R < 1 or R > Nk, or chunk index out of range                   */
+  RINGX_E_UNSUPPORTED = 4, /* dtype or head dim not supported (bf16: d in {64,128}; fp32: 1..128) */
+  RINGX_E_ALIGN = 5,       /* a tensor pointer is not 16-byte aligned                        */
+  RINGX_E_WORKSPACE = 6,   /* backward workspace missing or smaller than required            */
+  RINGX_E_HIP = 7,         /* a HIP launch failed                                            */
+  RINGX_E_ALIAS = 8        /* an output overlaps an input                                    */
+} ringx_status;
+
+typedef enum ringx_dtype { RINGX_FP32 = 0, RINGX_BF16 = 1 } ringx_dtype;
+
+/*
+ * Ring-chunked forward with the Eq. (5) merge fused (Sec. III-A, Eqs. (1)-(5)).
+ *   q [B,H,Nq,d], k [B,H,Nk,d], v [B,H,Nk,d] (dtype) -- inputs.
+ *   out [B,H,Nq,d] (dtype)  -- softmax(scale q k^T) v over all Nk keys.
+ *   lse [B,H,Nq] (fp32)     -- merged log-sum-exp, lse_max + log(den) of Eq. (5); the backward's
+ *                              input.
+ *   R -- number of ring-step chunks; each chunk's (loc_out, loc_lse) is formed and merged in
+ *   registers, in chunk order.
+ */
+ringx_status ringx_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                            float scale, ringx_dtype dtype, hipStream_t stream);
+
+/*
+ * Per-chunk forward without the merge: the R local results of Sec. III-A (loc_out_i, loc_lse_i
+ * "on the sequence chunk S_i"), as another GPU of a RingX_a group would produce them.
+ *   part_out [R,B,H,Nq,d] (fp32), part_lse [R,B,H,Nq] (fp32, natural log).
+ */
+ringx_status ringx_attn_fwd_partials(const void* q, const void* k, const void* v, float* part_out,
+                                     float* part_lse, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
+                                     int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                     hipStream_t stream);
+
+/*
+ * Standalone N-way merge of partial results, Eq. (5) (Sec. III-A: allreduce of lse_max, then the
+ * reduction of num and den; num/den is the attention):
+ *   lse_max = max_r part_lse[r];  w_r = exp(part_lse[r] - lse_max);
+ *   out = sum_r w_r part_out[r] / sum_r w_r;  lse = lse_max + log(sum_r w_r).
+ *   part_out [R,B,H,Nq,d] fp32, part_lse [R,B,H,Nq] fp32 -- inputs (a partial with lse = -inf
+ *   contributes nothing; every row needs one finite partial).
+ *   out [B,H,Nq,d] in out_dtype (bf16 or fp32), lse [B,H,Nq] fp32.
+ */
+ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void* out, float* lse,
+                             int64_t R, int64_t B, int64_t H, int64_t Nq, int64_t d,
+                             ringx_dtype out_dtype, hipStream_t stream);
+
+/*
+ * Recompute-based backward with the merged lse (Sec. III-A, "Communication scheme": K/V chunk
+ * gradients are computed per chunk, dQ accumulates over all N steps).  Softmax gradient:
+ *   D_i = sum_c dout_ic out_ic;  P_ij = exp(scale q_i.k_j - lse_i);  dP_ij = dout_i . v_j;
+ *   dS_ij = P_ij (dP_ij - D_i);  dV_j = sum_i P_ij dout_i;  dK_j = scale sum_i dS_ij q_i;
+ *   dQ_i = scale sum_j dS_ij k_j.
+ *   q, k, v, out, dout (dtype), lse [B,H,Nq] fp32 (from ringx_attn_fwd or ringx_lse_merge).
+ *   dq [B,H,Nq,d] fp32 -- overwritten; accumulated over every chunk in fp32.
+ *   dk, dv [B,H,Nk,d] fp32 -- overwritten, or added to when accumulate_dkv != 0 (as dK/dV
+ *   travelling around a ring collect the contributions of other query shards).
+ *   workspace/workspace_bytes -- device scratch of at least ringx_bwd_workspace_bytes(...) bytes,
+ *   16-byte aligned, owned by the caller; contents on entry are ignored.
+ *   R -- chunk count: no key tile straddles a chunk boundary; results do not depend on R beyond
+ *   rounding.  dq is not bitwise reproducible (fp32 atomics); dk, dv are.
+ */
+ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const void* out,
+                            const void* dout, const float* lse, float* dq, float* dk, float* dv,
+                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                            float scale, ringx_dtype dtype, int accumulate_dkv, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of backward workspace for these arguments (0 if the arguments are invalid).  Host only. */
+size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
+                                 int64_t R, ringx_dtype dtype);
+
+/* Key range [*lo, *hi) of chunk r (lo = floor(r*Nk/R)).  Host only; no HIP call. */
+ringx_status ringx_chunk_bounds(int64_t Nk, int64_t R, int64_t r, int64_t* lo, int64_t* hi);
+
+/* Static, NUL-terminated description of a status code. */
+const char* ringx_status_str(ringx_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RINGX_H */

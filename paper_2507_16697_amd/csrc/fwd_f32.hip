@@ -1,0 +1,121 @@
+// Ring-chunked attention forward in fp32 (storage and arithmetic), any head dim 1..128.
+//
+// The exactness path: one thread per query row, keys streamed through LDS in tiles of 32.  For
+// every chunk r the thread runs an online softmax over the chunk's keys (Eqs. (2)-(4) of arXiv
+// 2507.16697 Sec. III-A), forms the chunk's local result (loc_out_r, loc_lse_r), and either writes
+// it (partials mode) or folds it into the Eq. (5) merge.  The merged output accumulates in place in
+// the fp32 output row, which only this thread touches.
+
+#include "ringx_device.h"
+#include "ringx_kernels.h"
+
+namespace ringx {
+namespace {
+
+constexpr int kF32Threads = 128;
+constexpr int kF32Tile = 32;
+
+template <int DMAX, bool PARTIALS>
+__global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
+    const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
+    float* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
+    float* __restrict__ part_lse, int64_t BH, int64_t Nq, int64_t Nk, int R, int d, float scale) {
+  __shared__ float ks[kF32Tile * DMAX];
+  __shared__ float vs[kF32Tile * DMAX];
+  const int t = threadIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int64_t qi = (int64_t)blockIdx.x * kF32Threads + t;
+  const bool active = qi < Nq;
+  const float* kb = k + bh * Nk * d;
+  const float* vb = v + bh * Nk * d;
+
+  float qr[DMAX];
+#pragma unroll
+  for (int c = 0; c < DMAX; ++c) qr[c] = (active && c < d) ? q[(bh * Nq + qi) * d + c] : 0.f;
+  float* orow = out + (bh * Nq + (active ? qi : 0)) * d;
+
+  float lse_m = -INFINITY;
+  for (int r = 0; r < R; ++r) {
+    const int64_t lo = (int64_t)r * Nk / R;
+    const int64_t hi = (int64_t)(r + 1) * Nk / R;
+    float m = -INFINITY, l = 0.f;
+    float o[DMAX];
+#pragma unroll
+    for (int c = 0; c < DMAX; ++c) o[c] = 0.f;
+    for (int64_t j0 = lo; j0 < hi; j0 += kF32Tile) {
+      const int nk = (int)min<int64_t>(kF32Tile, hi - j0);
+      __syncthreads();
+      for (int idx = t; idx < nk * d; idx += kF32Threads) {
+        ks[(idx / d) * DMAX + idx % d] = kb[j0 * d + idx];
+        vs[(idx / d) * DMAX + idx % d] = vb[j0 * d + idx];
+      }
+      __syncthreads();
+      for (int j = 0; j < nk; ++j) {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < DMAX; ++c)
+          if (c < d) s = __builtin_fmaf(qr[c], ks[j * DMAX + c], s);
+        s *= scale;
+        const float mn = fmaxf(m, s);
+        const float alpha = expf(m - mn);
+        const float p = expf(s - mn);
+        l = l * alpha + p;
+#pragma unroll
+        for (int c = 0; c < DMAX; ++c)
+          if (c < d) o[c] = __builtin_fmaf(p, vs[j * DMAX + c], o[c] * alpha);
+        m = mn;
+      }
+    }
+    const float inv = 1.0f / l;
+    const float lse_r = m + logf(l);
+    if (!active) continue;
+    if constexpr (PARTIALS) {
+      float* po = part_out + (((int64_t)r * BH + bh) * Nq + qi) * d;
+#pragma unroll
+      for (int c = 0; c < DMAX; ++c)
+        if (c < d) po[c] = o[c] * inv;
+      part_lse[((int64_t)r * BH + bh) * Nq + qi] = lse_r;
+    } else {
+      // Eq. (5), streamed: fold (loc_out_r, loc_lse_r) into the merged row
+      const float M = fmaxf(lse_m, lse_r);
+      const float a = expf(lse_m - M);
+      const float b = expf(lse_r - M);
+      const float den = a + b;
+      const float wa = a / den;
+      const float wb = b * inv / den;
+#pragma unroll
+      for (int c = 0; c < DMAX; ++c)
+        if (c < d) orow[c] = (r == 0 ? 0.f : orow[c] * wa) + o[c] * wb;
+      lse_m = M + logf(den);
+    }
+  }
+  if constexpr (!PARTIALS) {
+    if (active) lse[bh * Nq + qi] = lse_m;
+  }
+}
+
+template <int DMAX>
+hipError_t launch(const FwdArgs& a, bool partials) {
+  dim3 grid((uint32_t)((a.Nq + kF32Threads - 1) / kF32Threads), (uint32_t)a.BH);
+  if (partials)
+    hipLaunchKernelGGL((fwd_f32_kernel<DMAX, true>), grid, dim3(kF32Threads), 0, a.stream,
+                       (const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.out,
+                       a.lse, a.part_out, a.part_lse, a.BH, a.Nq, a.Nk, (int)a.R, (int)a.d,
+                       a.scale);
+  else
+    hipLaunchKernelGGL((fwd_f32_kernel<DMAX, false>), grid, dim3(kF32Threads), 0, a.stream,
+                       (const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.out,
+                       a.lse, a.part_out, a.part_lse, a.BH, a.Nq, a.Nk, (int)a.R, (int)a.d,
+                       a.scale);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_fwd_f32(const FwdArgs& a, bool partials) {
+  if (a.d <= 32) return launch<32>(a, partials);
+  if (a.d <= 64) return launch<64>(a, partials);
+  return launch<128>(a, partials);
+}
+
+}  // namespace ringx

@@ -1,0 +1,93 @@
+// Standalone N-way merge of per-chunk partial results, Eq. (5) of arXiv 2507.16697 Sec. III-A.
+//
+//   lse_max = max_r part_lse[r]          (the paper's allreduce-max)
+//   w_r     = exp(part_lse[r] - lse_max)
+//   out     = sum_r w_r part_out[r] / sum_r w_r,   lse = lse_max + log(sum_r w_r)
+//
+// HBM-bound: each output row reads R fp32 rows of d values and R log-sum-exps once.  Vector path:
+// one thread per 4 consecutive columns of a row (16-byte loads, consecutive threads cover a row);
+// scalar path for head dims that are not a multiple of 4 (fp32 output only).
+
+#include "ringx_device.h"
+#include "ringx_kernels.h"
+
+namespace ringx {
+namespace {
+
+constexpr int kMergeThreads = 256;
+
+template <bool OUT_BF16>
+__global__ __launch_bounds__(kMergeThreads) void merge_vec4_kernel(
+    const float* __restrict__ part_out, const float* __restrict__ part_lse, void* __restrict__ out,
+    float* __restrict__ lse, int R, int64_t rows, int d) {
+  const int quads = d >> 2;
+  const int64_t idx = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
+  if (idx >= rows * quads) return;
+  const int64_t row = idx / quads;
+  const int c = (int)(idx % quads) * 4;
+
+  float M = -INFINITY;
+  for (int r = 0; r < R; ++r) M = fmaxf(M, part_lse[(int64_t)r * rows + row]);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float den = 0.f;
+  for (int r = 0; r < R; ++r) {
+    const float w = fast_exp2((part_lse[(int64_t)r * rows + row] - M) * kLog2e);
+    const f32x4 x = *reinterpret_cast<const f32x4*>(part_out + ((int64_t)r * rows + row) * d + c);
+    acc += x * w;
+    den += w;
+  }
+  const float inv = 1.0f / den;
+  acc *= inv;
+  if constexpr (OUT_BF16) {
+    u32x2 w2;
+    w2[0] = pack_bf16x2(acc[0], acc[1]);
+    w2[1] = pack_bf16x2(acc[2], acc[3]);
+    *reinterpret_cast<u32x2*>(reinterpret_cast<__bf16*>(out) + row * d + c) = w2;
+  } else {
+    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(out) + row * d + c) = acc;
+  }
+  if (c == 0) lse[row] = M + logf(den);
+}
+
+__global__ __launch_bounds__(kMergeThreads) void merge_scalar_kernel(
+    const float* __restrict__ part_out, const float* __restrict__ part_lse,
+    float* __restrict__ out, float* __restrict__ lse, int R, int64_t rows, int d) {
+  const int64_t idx = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
+  if (idx >= rows * d) return;
+  const int64_t row = idx / d;
+  const int c = (int)(idx % d);
+  float M = -INFINITY;
+  for (int r = 0; r < R; ++r) M = fmaxf(M, part_lse[(int64_t)r * rows + row]);
+  float acc = 0.f, den = 0.f;
+  for (int r = 0; r < R; ++r) {
+    const float w = expf(part_lse[(int64_t)r * rows + row] - M);
+    acc = __builtin_fmaf(w, part_out[((int64_t)r * rows + row) * d + c], acc);
+    den += w;
+  }
+  out[row * d + c] = acc / den;
+  if (c == 0) lse[row] = M + logf(den);
+}
+
+}  // namespace
+
+hipError_t launch_lse_merge(const MergeArgs& a) {
+  const int64_t rows = a.BH * a.Nq;
+  if (a.d % 4 == 0) {
+    const int64_t n = rows * (a.d / 4);
+    const dim3 grid((uint32_t)((n + kMergeThreads - 1) / kMergeThreads));
+    if (a.out_bf16)
+      hipLaunchKernelGGL(merge_vec4_kernel<true>, grid, dim3(kMergeThreads), 0, a.stream,
+                         a.part_out, a.part_lse, a.out, a.lse, (int)a.R, rows, (int)a.d);
+    else
+      hipLaunchKernelGGL(merge_vec4_kernel<false>, grid, dim3(kMergeThreads), 0, a.stream,
+                         a.part_out, a.part_lse, a.out, a.lse, (int)a.R, rows, (int)a.d);
+  } else {
+    const int64_t n = rows * a.d;
+    const dim3 grid((uint32_t)((n + kMergeThreads - 1) / kMergeThreads));
+    hipLaunchKernelGGL(merge_scalar_kernel, grid, dim3(kMergeThreads), 0, a.stream, a.part_out,
+                       a.part_lse, (float*)a.out, a.lse, (int)a.R, rows, (int)a.d);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ringx

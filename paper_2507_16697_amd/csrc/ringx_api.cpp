@@ -1,0 +1,203 @@
+// C ABI of libringx (declared in include/ringx.h): host-side validation, workspace sizing and
+// kernel dispatch.  Every check runs before the first HIP call, so an error status means nothing
+// was enqueued and no output was touched.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "ringx.h"
+#include "ringx_kernels.h"
+
+namespace {
+
+constexpr int64_t kMaxElems = int64_t(1) << 40;   // per tensor; keeps every index product in int64
+constexpr int64_t kMaxRowsF32 = 65535;            // fp32 kernels put B*H on grid.y
+constexpr int64_t kMaxKeys = int64_t(1) << 31;    // keeps r * Nk (chunk bounds) inside int64
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Span {
+  uintptr_t lo, hi;
+};
+Span span(const void* p, int64_t bytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return Span{a, a + static_cast<uintptr_t>(bytes)};
+}
+bool overlap(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
+
+int64_t esize(ringx_dtype t) { return t == RINGX_BF16 ? 2 : 4; }
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > kMaxElems / a) return false;
+  *out = a * b;
+  return *out <= kMaxElems;
+}
+
+ringx_status check_dims(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                        float scale, ringx_dtype dtype) {
+  if (B < 1 || H < 1 || Nq < 1 || Nk < 1 || Nk > kMaxKeys) return RINGX_E_SHAPE;
+  if (!(std::isfinite(scale) && scale > 0.f)) return RINGX_E_SHAPE;
+  if (dtype != RINGX_BF16 && dtype != RINGX_FP32) return RINGX_E_UNSUPPORTED;
+  if (dtype == RINGX_BF16 && d != 64 && d != 128) return RINGX_E_UNSUPPORTED;
+  if (dtype == RINGX_FP32 && (d < 1 || d > 128)) return RINGX_E_UNSUPPORTED;
+  if (R < 1 || R > Nk) return RINGX_E_CHUNKS;
+  int64_t bh, x;
+  if (!mul_ok(B, H, &bh)) return RINGX_E_SHAPE;
+  if (dtype == RINGX_FP32 && bh > kMaxRowsF32) return RINGX_E_SHAPE;
+  if (!mul_ok(bh, Nq, &x) || !mul_ok(x, d, &x) || !mul_ok(x, R, &x)) return RINGX_E_SHAPE;
+  if (!mul_ok(bh, Nk, &x) || !mul_ok(x, d, &x)) return RINGX_E_SHAPE;
+  if (dtype == RINGX_BF16 && ringx::fwd_bf16_workgroups(bh, Nq, d) > 0xffffffffll)
+    return RINGX_E_SHAPE;
+  // the backward grid: one workgroup per (b, h, chunk, 128-key tile)
+  if (dtype == RINGX_BF16) {
+    const int64_t tpc = ((Nk + R - 1) / R + 127) / 128;
+    if (!mul_ok(bh, R, &x) || !mul_ok(x, tpc, &x) || x > 0xffffffffll) return RINGX_E_SHAPE;
+  }
+  return RINGX_OK;
+}
+
+ringx_status hip_status(hipError_t e) { return e == hipSuccess ? RINGX_OK : RINGX_E_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* ringx_status_str(ringx_status s) {
+  switch (s) {
+    case RINGX_OK: return "ok";
+    case RINGX_E_NULLPTR: return "a required pointer is NULL";
+    case RINGX_E_SHAPE: return "invalid shape, size overflow or scale";
+    case RINGX_E_CHUNKS: return "chunk count or index out of range (need 1 <= R <= Nk)";
+    case RINGX_E_UNSUPPORTED: return "unsupported dtype or head dim";
+    case RINGX_E_ALIGN: return "tensor pointer not 16-byte aligned";
+    case RINGX_E_WORKSPACE: return "backward workspace missing or too small";
+    case RINGX_E_HIP: return "HIP launch failed";
+    case RINGX_E_ALIAS: return "an output overlaps an input";
+  }
+  return "unknown status";
+}
+
+ringx_status ringx_chunk_bounds(int64_t Nk, int64_t R, int64_t r, int64_t* lo, int64_t* hi) {
+  if (!lo || !hi) return RINGX_E_NULLPTR;
+  if (Nk < 1 || Nk > kMaxElems) return RINGX_E_SHAPE;
+  if (R < 1 || R > Nk || r < 0 || r >= R) return RINGX_E_CHUNKS;
+  // r * Nk < 2^40 * 2^40 would overflow int64 for extreme inputs; split the product
+  const int64_t qn = Nk / R, rn = Nk % R;
+  *lo = r * qn + (r * rn) / R;
+  *hi = (r + 1) * qn + ((r + 1) * rn) / R;
+  return RINGX_OK;
+}
+
+ringx_status ringx_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                            float scale, ringx_dtype dtype, hipStream_t stream) {
+  if (!q || !k || !v || !out || !lse) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(lse))
+    return RINGX_E_ALIGN;
+  const int64_t es = esize(dtype), bh = B * H;
+  const Span sq = span(q, bh * Nq * d * es), sk = span(k, bh * Nk * d * es),
+             sv = span(v, bh * Nk * d * es);
+  const Span so = span(out, bh * Nq * d * es), sl = span(lse, bh * Nq * 4);
+  for (Span o : {so, sl})
+    for (Span i : {sq, sk, sv})
+      if (overlap(o, i)) return RINGX_E_ALIAS;
+  if (overlap(so, sl)) return RINGX_E_ALIAS;
+  ringx::FwdArgs a{q, k, v, out, lse, nullptr, nullptr, bh, Nq, Nk, d, R, scale, stream};
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, false)
+                                        : ringx::launch_fwd_f32(a, false));
+}
+
+ringx_status ringx_attn_fwd_partials(const void* q, const void* k, const void* v, float* part_out,
+                                     float* part_lse, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
+                                     int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                     hipStream_t stream) {
+  if (!q || !k || !v || !part_out || !part_lse) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(part_out) ||
+      !aligned16(part_lse))
+    return RINGX_E_ALIGN;
+  const int64_t es = esize(dtype), bh = B * H;
+  const Span sq = span(q, bh * Nq * d * es), sk = span(k, bh * Nk * d * es),
+             sv = span(v, bh * Nk * d * es);
+  const Span so = span(part_out, R * bh * Nq * d * 4), sl = span(part_lse, R * bh * Nq * 4);
+  for (Span o : {so, sl})
+    for (Span i : {sq, sk, sv})
+      if (overlap(o, i)) return RINGX_E_ALIAS;
+  if (overlap(so, sl)) return RINGX_E_ALIAS;
+  ringx::FwdArgs a{q, k, v, nullptr, nullptr, part_out, part_lse, bh, Nq, Nk, d, R, scale, stream};
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, true)
+                                        : ringx::launch_fwd_f32(a, true));
+}
+
+ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void* out, float* lse,
+                             int64_t R, int64_t B, int64_t H, int64_t Nq, int64_t d,
+                             ringx_dtype out_dtype, hipStream_t stream) {
+  if (!part_out || !part_lse || !out || !lse) return RINGX_E_NULLPTR;
+  if (B < 1 || H < 1 || Nq < 1) return RINGX_E_SHAPE;
+  if (R < 1) return RINGX_E_CHUNKS;
+  if (out_dtype != RINGX_BF16 && out_dtype != RINGX_FP32) return RINGX_E_UNSUPPORTED;
+  if (d < 1 || d > 128 || (out_dtype == RINGX_BF16 && d % 4 != 0)) return RINGX_E_UNSUPPORTED;
+  int64_t bh, x;
+  if (!mul_ok(B, H, &bh) || !mul_ok(bh, Nq, &x) || !mul_ok(x, d, &x) || !mul_ok(x, R, &x))
+    return RINGX_E_SHAPE;
+  if ((bh * Nq * d + 255) / 256 > 0xffffffffll) return RINGX_E_SHAPE;
+  if (!aligned16(part_out) || !aligned16(part_lse) || !aligned16(out) || !aligned16(lse))
+    return RINGX_E_ALIGN;
+  const Span si = span(part_out, R * bh * Nq * d * 4), sil = span(part_lse, R * bh * Nq * 4);
+  const Span so = span(out, bh * Nq * d * esize(out_dtype)), sl = span(lse, bh * Nq * 4);
+  for (Span o : {so, sl})
+    for (Span i : {si, sil})
+      if (overlap(o, i)) return RINGX_E_ALIAS;
+  if (overlap(so, sl)) return RINGX_E_ALIAS;
+  ringx::MergeArgs a{part_out, part_lse, out, lse, R, bh, Nq, d, out_dtype == RINGX_BF16, stream};
+  return hip_status(ringx::launch_lse_merge(a));
+}
+
+size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
+                                 int64_t R, ringx_dtype dtype) {
+  if (check_dims(B, H, Nq, Nk, d, R, 1.0f, dtype) != RINGX_OK) return 0;
+  const int64_t delta = B * H * Nq * 4;
+  return static_cast<size_t>((delta + 255) / 256 * 256);
+}
+
+ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const void* out,
+                            const void* dout, const float* lse, float* dq, float* dk, float* dv,
+                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                            float scale, ringx_dtype dtype, int accumulate_dkv, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  const size_t need = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, dtype);
+  if (!workspace || workspace_bytes < need) return RINGX_E_WORKSPACE;
+  for (const void* p : {q, k, v, out, dout, (const void*)lse, (const void*)dq, (const void*)dk,
+                        (const void*)dv, (const void*)workspace})
+    if (!aligned16(p)) return RINGX_E_ALIGN;
+  const int64_t es = esize(dtype), bh = B * H;
+  const Span ins[] = {span(q, bh * Nq * d * es),    span(k, bh * Nk * d * es),
+                      span(v, bh * Nk * d * es),    span(out, bh * Nq * d * es),
+                      span(dout, bh * Nq * d * es), span(lse, bh * Nq * 4)};
+  const Span outs[] = {span(dq, bh * Nq * d * 4), span(dk, bh * Nk * d * 4),
+                       span(dv, bh * Nk * d * 4), span(workspace, (int64_t)need)};
+  for (int i = 0; i < 4; ++i) {
+    for (const Span& s : ins)
+      if (overlap(outs[i], s)) return RINGX_E_ALIAS;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], outs[j])) return RINGX_E_ALIAS;
+  }
+  ringx::BwdArgs a{q,  k,  v,  out, dout, lse,   dq, dk, dv, static_cast<float*>(workspace),
+                   bh, Nq, Nk, d,   R,    scale, accumulate_dkv != 0, stream};
+  const bool bf16 = dtype == RINGX_BF16;
+  hipError_t e = ringx::launch_bwd_pre(a, bf16);
+  if (e != hipSuccess) return RINGX_E_HIP;
+  return hip_status(bf16 ? ringx::launch_bwd_bf16(a) : ringx::launch_bwd_f32(a));
+}
+
+}  // extern "C"

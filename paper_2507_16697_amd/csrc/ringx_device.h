@@ -1,0 +1,59 @@
+// Device-side helpers shared by the libringx kernels (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ringx {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// v_mfma_f32_32x32x16_bf16.  Operand layout for lane l (g = l / 32, n = l % 32):
+//   A (32 x 16): row n, k = 8g .. 8g+7      B (16 x 32): column n, k = 8g .. 8g+7
+//   C (32 x 32): column n, rows 8*(r/4) + 4g + (r%4) for accumulator r = 0..15
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// fp32 pair -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  f32x2 x = {lo, hi};
+  bf16x2 y = __builtin_convertvector(x, bf16x2);
+  return __builtin_bit_cast(uint32_t, y);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Value held by lane (l ^ 32), exchanged with v_permlane32_swap.
+__device__ __forceinline__ float swap_half(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]);
+}
+
+// Logical workgroup id so that the workgroups resident on one XCD work on the same (b, h) slice.
+// The hardware hands consecutive workgroup ids to the 8 XCDs round robin; this groups id w's
+// XCD (w % 8) onto a contiguous range of logical ids.
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t w, uint32_t n) {
+  constexpr uint32_t kXcd = 8;
+  const uint32_t per = n / kXcd;           // full rounds
+  const uint32_t full = per * kXcd;
+  if (w >= full) return w;                 // ragged last round keeps its id
+  return (w % kXcd) * per + w / kXcd;
+}
+
+}  // namespace ringx

@@ -1,0 +1,211 @@
+"""Thin Python binding of libringx (C ABI in include/ringx.h).
+
+Argument marshalling only: every step of the attention runs in the library's HIP kernels.  torch
+supplies device memory and the current HIP stream.  Function names follow the C entry points.
+
+    out, lse = ringx_attn_fwd(q, k, v, R)                     # q,k,v: [B,H,N,d] cuda tensors
+    part_out, part_lse = ringx_attn_fwd_partials(q, k, v, R)
+    out, lse = ringx_lse_merge(part_out, part_lse, out_dtype=torch.bfloat16)
+    dq, dk, dv = ringx_attn_bwd(q, k, v, out, dout, lse, R)
+
+The library must be built (``python -m paper_2507_16697_amd.build``); loading fails loudly if it
+is missing -- there is no fallback implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libringx.so")
+
+RINGX_FP32 = 0
+RINGX_BF16 = 1
+
+STATUS_NAMES = {
+    0: "RINGX_OK", 1: "RINGX_E_NULLPTR", 2: "RINGX_E_SHAPE", 3: "RINGX_E_CHUNKS",
+    4: "RINGX_E_UNSUPPORTED", 5: "RINGX_E_ALIGN", 6: "RINGX_E_WORKSPACE", 7: "RINGX_E_HIP",
+    8: "RINGX_E_ALIAS",
+}
+
+EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "ringx_attn_bwd",
+            "ringx_bwd_workspace_bytes", "ringx_chunk_bounds", "ringx_status_str")
+
+
+class RingxError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)} ({message})")
+        self.status = status
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int64
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libringx.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libringx.so not found at {LIB_PATH}; build it with "
+                               "`python -m paper_2507_16697_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.ringx_attn_fwd.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, ctypes.c_float,
+                                     ctypes.c_int, _P]
+        L.ringx_attn_fwd_partials.argtypes = L.ringx_attn_fwd.argtypes
+        L.ringx_lse_merge.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, _I, ctypes.c_int, _P]
+        L.ringx_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
+                                     ctypes.c_float, ctypes.c_int, ctypes.c_int, _P,
+                                     ctypes.c_size_t, _P]
+        L.ringx_bwd_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, ctypes.c_int]
+        L.ringx_bwd_workspace_bytes.restype = ctypes.c_size_t
+        L.ringx_chunk_bounds.argtypes = [_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
+        L.ringx_status_str.argtypes = [ctypes.c_int]
+        L.ringx_status_str.restype = ctypes.c_char_p
+        for name in ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge",
+                     "ringx_attn_bwd", "ringx_chunk_bounds"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def ringx_status_str(status: int) -> str:
+    return lib().ringx_status_str(int(status)).decode()
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise RingxError(fn, status, ringx_status_str(status))
+
+
+def ringx_chunk_bounds(Nk: int, R: int, r: int) -> tuple[int, int]:
+    lo, hi = _I(), _I()
+    _check("ringx_chunk_bounds", lib().ringx_chunk_bounds(Nk, R, r, ctypes.byref(lo), ctypes.byref(hi)))
+    return lo.value, hi.value
+
+
+def ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, dtype) -> int:
+    return int(lib().ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, int(dtype)))
+
+
+# ---------------------------------------------------------------------------------------------
+# torch tensor helpers
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return RINGX_BF16
+    if t.dtype == torch.float32:
+        return RINGX_FP32
+    raise TypeError(f"unsupported dtype {t.dtype}; expected bfloat16 or float32")
+
+
+def _dev(*ts):
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("tensors must live on the GPU")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous [B, H, N, d]")
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if hasattr(stream, "cuda_stream"):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _scale(scale, d):
+    return float(1.0 / math.sqrt(d)) if scale is None else float(scale)
+
+
+def ringx_attn_fwd(q, k, v, R: int, scale=None, out=None, lse=None, stream=None):
+    """Merged ring-chunked forward.  Returns (out [B,H,Nq,d] in q's dtype, lse [B,H,Nq] fp32)."""
+    torch = _torch()
+    _dev(q, k, v)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
+    _dev(out, lse)
+    st = lib().ringx_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                              lse.data_ptr(), B, H, Nq, Nk, d, R, _scale(scale, d),
+                              _dtype_code(q), _stream(stream))
+    _check("ringx_attn_fwd", st)
+    return out, lse
+
+
+def ringx_attn_fwd_partials(q, k, v, R: int, scale=None, part_out=None, part_lse=None,
+                            stream=None):
+    """Per-chunk local results: (part_out [R,B,H,Nq,d] fp32, part_lse [R,B,H,Nq] fp32)."""
+    torch = _torch()
+    _dev(q, k, v)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    if part_out is None:
+        part_out = torch.empty((R, B, H, Nq, d), dtype=torch.float32, device=q.device)
+    if part_lse is None:
+        part_lse = torch.empty((R, B, H, Nq), dtype=torch.float32, device=q.device)
+    _dev(part_out, part_lse)
+    st = lib().ringx_attn_fwd_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                       part_out.data_ptr(), part_lse.data_ptr(), B, H, Nq, Nk, d,
+                                       R, _scale(scale, d), _dtype_code(q), _stream(stream))
+    _check("ringx_attn_fwd_partials", st)
+    return part_out, part_lse
+
+
+def ringx_lse_merge(part_out, part_lse, out_dtype=None, out=None, lse=None, stream=None):
+    """Eq. (5) merge of R partials.  Returns (out [B,H,Nq,d] in out_dtype, lse [B,H,Nq] fp32)."""
+    torch = _torch()
+    _dev(part_out, part_lse)
+    R, B, H, Nq, d = part_out.shape
+    if out is None:
+        out = torch.empty((B, H, Nq, d), dtype=out_dtype or torch.float32, device=part_out.device)
+    if lse is None:
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=part_out.device)
+    _dev(out, lse)
+    st = lib().ringx_lse_merge(part_out.data_ptr(), part_lse.data_ptr(), out.data_ptr(),
+                               lse.data_ptr(), R, B, H, Nq, d, _dtype_code(out), _stream(stream))
+    _check("ringx_lse_merge", st)
+    return out, lse
+
+
+def ringx_attn_bwd(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None, dv=None,
+                   accumulate_dkv=False, workspace=None, stream=None):
+    """Recompute backward.  Returns fp32 (dq, dk, dv); dk/dv are added to when accumulate_dkv."""
+    torch = _torch()
+    _dev(q, k, v, out, dout, lse)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    f32 = dict(dtype=torch.float32, device=q.device)
+    if dq is None:
+        dq = torch.empty((B, H, Nq, d), **f32)
+    if dk is None:
+        dk = torch.zeros((B, H, Nk, d), **f32) if accumulate_dkv else torch.empty((B, H, Nk, d), **f32)
+    if dv is None:
+        dv = torch.zeros((B, H, Nk, d), **f32) if accumulate_dkv else torch.empty((B, H, Nk, d), **f32)
+    code = _dtype_code(q)
+    need = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, code)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _dev(dq, dk, dv, workspace)
+    st = lib().ringx_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                              dout.data_ptr(), lse.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                              dv.data_ptr(), B, H, Nq, Nk, d, R, _scale(scale, d), code,
+                              1 if accumulate_dkv else 0, workspace.data_ptr(),
+                              workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("ringx_attn_bwd", st)
+    return dq, dk, dv

@@ -1,0 +1,133 @@
+"""libringx on the host: it loads, exports every symbol include/ringx.h declares, and rejects bad
+arguments before any HIP call (no GPU needed: every call here fails validation or is host-only)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import attention_fp64 as oa
+from paper_2507_16697_amd import ringx
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ringx.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(ringx.LIB_PATH),
+                                reason="libringx.so not built (run python -m paper_2507_16697_amd.build)")
+
+OK, NULLPTR, SHAPE, CHUNKS, UNSUP, ALIGN, WORKSPACE, HIP, ALIAS = range(9)
+BF16, FP32 = ringx.RINGX_BF16, ringx.RINGX_FP32
+
+# Fake, never dereferenced device addresses: validation rejects every call below before any HIP
+# call, so these are only compared and aligned, never used.
+GB = 1 << 30
+QP, KP, VP, OP, LP = (0x10_0000_0000 + i * 64 * GB for i in range(5))
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:ringx_status|size_t|const char\*)\s+(ringx_\w+)\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    assert declared_functions() == sorted(ringx.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ringx.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for code in range(9):
+        s = ringx.ringx_status_str(code)
+        assert isinstance(s, str) and s
+    assert ringx.ringx_status_str(OK) == "ok"
+    assert ringx.ringx_status_str(1234) == "unknown status"
+
+
+def test_chunk_bounds_equal_the_oracle_formula():
+    for nk in list(range(1, 130)) + [1000, 4097, 262144, 524288]:
+        for R in sorted({1, 2, 3, 7, 8, nk // 2 or 1, nk}):
+            if R > nk:
+                continue
+            for r in range(R) if R <= 64 else (0, 1, R // 2, R - 1):
+                assert ringx.ringx_chunk_bounds(nk, R, r) == oa.chunk_bounds(nk, R, r)
+
+
+def test_chunk_bounds_huge_does_not_overflow():
+    nk = (1 << 40) - 3
+    R = 7
+    prev = 0
+    for r in range(R):
+        lo, hi = ringx.ringx_chunk_bounds(nk, R, r)
+        assert lo == prev and hi == ((r + 1) * nk) // R
+        prev = hi
+
+
+@pytest.mark.parametrize("args,code", [((5, 0, 0), CHUNKS), ((5, 6, 0), CHUNKS), ((5, 2, 2), CHUNKS),
+                                       ((5, 2, -1), CHUNKS), ((0, 1, 0), SHAPE)])
+def test_chunk_bounds_errors(args, code):
+    with pytest.raises(ringx.RingxError) as e:
+        ringx.ringx_chunk_bounds(*args)
+    assert e.value.status == code
+
+
+def fwd(q=QP, k=KP, v=VP, o=OP, l=LP, B=1, H=2, Nq=100, Nk=300, d=64, R=3, scale=0.125, dt=BF16):
+    return ringx.lib().ringx_attn_fwd(q, k, v, o, l, B, H, Nq, Nk, d, R, scale, dt, None)
+
+
+def part(q=QP, k=KP, v=VP, o=OP, l=LP, B=1, H=2, Nq=100, Nk=300, d=64, R=3, scale=0.125, dt=BF16):
+    return ringx.lib().ringx_attn_fwd_partials(q, k, v, o, l, B, H, Nq, Nk, d, R, scale, dt, None)
+
+
+@pytest.mark.parametrize("fn", [fwd, part])
+def test_forward_validation(fn):
+    assert fn(q=0) == NULLPTR and fn(l=0) == NULLPTR and fn(o=0) == NULLPTR
+    assert fn(B=0) == SHAPE and fn(H=-1) == SHAPE and fn(Nq=0) == SHAPE and fn(Nk=0) == SHAPE
+    assert fn(Nk=(1 << 31) + 1, R=1) == SHAPE
+    assert fn(scale=0.0) == SHAPE and fn(scale=float("nan")) == SHAPE and fn(scale=float("inf")) == SHAPE
+    assert fn(scale=-1.0) == SHAPE
+    assert fn(R=0) == CHUNKS and fn(R=301) == CHUNKS
+    assert fn(d=96) == UNSUP and fn(d=32) == UNSUP and fn(d=256) == UNSUP
+    assert fn(d=129, dt=FP32) == UNSUP and fn(d=0, dt=FP32) == UNSUP
+    assert fn(dt=7) == UNSUP
+    assert fn(q=QP + 8) == ALIGN and fn(o=OP + 2) == ALIGN and fn(l=LP + 4) == ALIGN
+    assert fn(o=QP) == ALIAS and fn(l=KP + 1024) == ALIAS and fn(l=OP) == ALIAS
+    assert fn(B=1 << 20, H=1 << 20, Nq=1 << 20) == SHAPE          # size overflow
+    assert fn(B=70000, dt=FP32, H=1) == SHAPE                       # fp32 grid limit
+
+
+def merge(po=QP, pl=KP, o=OP, l=LP, R=3, B=1, H=2, Nq=100, d=64, dt=BF16):
+    return ringx.lib().ringx_lse_merge(po, pl, o, l, R, B, H, Nq, d, dt, None)
+
+
+def test_merge_validation():
+    assert merge(po=0) == NULLPTR and merge(l=0) == NULLPTR
+    assert merge(R=0) == CHUNKS
+    assert merge(B=0) == SHAPE and merge(Nq=0) == SHAPE
+    assert merge(d=0) == UNSUP and merge(d=130) == UNSUP and merge(d=6) == UNSUP
+    assert merge(dt=5) == UNSUP
+    assert merge(po=QP + 4) == ALIGN
+    assert merge(o=QP) == ALIAS and merge(l=KP) == ALIAS
+
+
+def bwd(ws=VP + 32 * GB, wsb=1 << 20, dq=OP, dk=OP + 8 * GB, dv=OP + 16 * GB, acc=0, B=1, H=2,
+        Nq=100, Nk=300, d=64, R=3, dt=BF16, q=QP, lse=LP):
+    return ringx.lib().ringx_attn_bwd(q, KP, VP, QP + 8 * GB, QP + 16 * GB, lse, dq, dk, dv, B, H,
+                                      Nq, Nk, d, R, 0.125, dt, acc, ws, wsb, None)
+
+
+def test_backward_validation():
+    need = ringx.ringx_bwd_workspace_bytes(1, 2, 100, 300, 64, 3, BF16)
+    assert need >= 2 * 100 * 4 and need % 256 == 0
+    assert ringx.ringx_bwd_workspace_bytes(1, 2, 100, 300, 96, 3, BF16) == 0
+    assert bwd(q=0) == NULLPTR and bwd(dq=0) == NULLPTR and bwd(lse=0) == NULLPTR
+    assert bwd(ws=0) == WORKSPACE and bwd(wsb=need - 1) == WORKSPACE
+    assert bwd(R=301) == CHUNKS and bwd(d=80) == UNSUP and bwd(B=0) == SHAPE
+    assert bwd(dq=OP + 4) == ALIGN and bwd(ws=VP + 32 * GB + 8) == ALIGN
+    assert bwd(dq=QP) == ALIAS                      # dq over q
+    assert bwd(dk=OP) == ALIAS                      # dk over dq
+    assert bwd(ws=OP + 16 * GB) == ALIAS            # workspace over dv

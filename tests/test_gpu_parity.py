@@ -1,0 +1,316 @@
+"""HIP path against the fp64 oracle, through the C ABI (needs an MI355X).
+
+Sizes span several tiles with ragged tails (query tiles of 128, key tiles of 64/128 inside every
+chunk, chunk boundaries that are not tile aligned), plus the degenerate cases (one query, one key,
+R = 1, R = Nk).
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import attention_fp64 as oa
+from paper_2507_16697_amd import inputs, ringx
+
+from parity_util import (TOL_BF16_LSE, TOL_BF16_REL_RMS, TOL_F32, max_abs_err, random_case,
+                         rel_rms_err, to_device, to_host_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(t, store):
+    return {k: to_device(v, store) for k, v in t.items()}
+
+
+def _report(name, **errs):
+    print(name, " ".join(f"{k}={v:.3e}" for k, v in errs.items()), flush=True)
+
+
+# ----------------------------------------------------------------------------------------------
+# fp32 exactness path
+
+
+def test_fp32_exact_workload():
+    """1024 queries x 1024 keys, H=2, d=64, R=4, fp32 i.i.d. N(0,1) from seed 0."""
+    w = inputs.WORKLOADS["exact_fp32_n1k"]
+    t = inputs.make_workload(w.name, use_cache=False)
+    x = {k: inputs.to_f64(v, "fp32") for k, v in t.items()}
+    g = _dev(t, "fp32")
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], w.R, scale=w.scale)
+    po, pl = ringx.ringx_attn_fwd_partials(g["q"], g["k"], g["v"], w.R, scale=w.scale)
+    mo, ml = ringx.ringx_lse_merge(po, pl, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref_po, ref_pl = oracle.attention_partials(x["q"], x["k"], x["v"], w.scale, w.R)
+    ref_o, ref_l = oa.lse_merge(ref_po, ref_pl)
+    errs = dict(out=max_abs_err(to_host_f64(out), ref_o), lse=max_abs_err(to_host_f64(lse), ref_l),
+                part_out=max_abs_err(to_host_f64(po), ref_po),
+                part_lse=max_abs_err(to_host_f64(pl), ref_pl),
+                merged_out=max_abs_err(to_host_f64(mo), ref_o),
+                merged_lse=max_abs_err(to_host_f64(ml), ref_l))
+    _report("exact_fp32_n1k", **errs)
+    for k, e in errs.items():
+        assert e <= TOL_F32, (k, e)
+
+
+@pytest.mark.parametrize("B,H,Nq,Nk,d,R", [(1, 1, 1, 1, 1, 1), (2, 3, 37, 101, 3, 5),
+                                           (1, 2, 130, 65, 128, 65), (1, 1, 300, 200, 100, 3),
+                                           (2, 1, 129, 33, 64, 1)])
+def test_fp32_shapes(B, H, Nq, Nk, d, R):
+    t, x = random_case(7, B, H, Nq, Nk, d, store="fp32")
+    g = _dev(t, "fp32")
+    scale = float(np.float32(1 / math.sqrt(d)))
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle.attention_chunked(x["q"], x["k"], x["v"], scale, R)
+    assert max_abs_err(to_host_f64(out), ref_o) <= TOL_F32
+    assert max_abs_err(to_host_f64(lse), ref_l) <= TOL_F32
+
+
+def test_fp32_backward():
+    B, H, Nq, Nk, d, R = 1, 2, 70, 90, 16, 3
+    t, x = random_case(8, B, H, Nq, Nk, d, store="fp32")
+    g = _dev(t, "fp32")
+    scale = 0.25
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle.attention(x["q"], x["k"], x["v"], scale)
+    rq, rk, rv = oracle.attention_bwd(x["q"], x["k"], x["v"], ref_o, x["do"], ref_l, scale)
+    for name, got, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        e = max_abs_err(to_host_f64(got), ref)
+        _report("fp32 bwd " + name, err=e)
+        assert e <= TOL_F32 * max(1.0, float(np.max(np.abs(ref)))), (name, e)
+
+
+# ----------------------------------------------------------------------------------------------
+# chunk bookkeeping: exact
+
+
+def test_chunk_coverage_probe_fp32():
+    """Q = 0, v_j = (j, 1): chunk r's local result is the mean key index of [lo_r, hi_r) and
+    lse = ln(hi_r - lo_r), which identifies the key range exactly."""
+    Nq, Nk, d = 5, 1000, 2
+    for R in (1, 3, 7, 64):
+        q = torch.zeros((1, 1, Nq, d), device="cuda")
+        k = torch.randn((1, 1, Nk, d), device="cuda")
+        v = torch.stack([torch.arange(Nk, dtype=torch.float32), torch.ones(Nk)], dim=-1)
+        v = v.reshape(1, 1, Nk, d).cuda()
+        po, pl = ringx.ringx_attn_fwd_partials(q, k, v, R, scale=1.0)
+        po, pl = po.cpu().numpy(), pl.cpu().numpy()
+        for r in range(R):
+            n = int(round(math.exp(float(pl[r, 0, 0, 0]))))
+            lo = int(round(float(po[r, 0, 0, 0, 0]) - (n - 1) / 2))
+            assert (lo, lo + n) == oa.chunk_bounds(Nk, R, r), (R, r)
+            assert np.all(po[r, 0, 0, :, 1] == 1.0)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_chunk_coverage_probe_bf16(d):
+    """bf16 variant: with Q = 0 every probability is exactly 1, V carries j % 256 and j // 256
+    (exact in bf16), so the fp32 partials give the sum of key indices of each chunk."""
+    Nq, Nk = 3, 4000
+    j = torch.arange(Nk, dtype=torch.float32)
+    v = torch.zeros((1, 1, Nk, d))
+    v[0, 0, :, 0] = j % 256
+    v[0, 0, :, 1] = torch.div(j, 256, rounding_mode="floor")
+    v[0, 0, :, 2] = 1.0
+    v = v.to(torch.bfloat16).cuda()
+    q = torch.zeros((1, 1, Nq, d), dtype=torch.bfloat16, device="cuda")
+    k = torch.randn((1, 1, Nk, d), device="cuda").to(torch.bfloat16)
+    for R in (1, 3, 8, 61):
+        po, pl = ringx.ringx_attn_fwd_partials(q, k, v, R, scale=0.1)
+        po, pl = po.double().cpu().numpy(), pl.double().cpu().numpy()
+        for r in range(R):
+            n = int(round(math.exp(pl[r, 0, 0, 0])))
+            s = round(po[r, 0, 0, 0, 0] * n) + 256 * round(po[r, 0, 0, 0, 1] * n)
+            lo = (s - n * (n - 1) // 2) // n
+            assert (lo, lo + n) == oa.chunk_bounds(Nk, R, r), (d, R, r)
+            assert np.allclose(po[r, 0, 0, :, 2], 1.0, rtol=0, atol=1e-6)
+
+
+# ----------------------------------------------------------------------------------------------
+# bf16 MFMA path
+
+
+BF16_SHAPES = [
+    # B, H, Nq, Nk, d, R
+    (1, 2, 300, 1000, 64, 3),
+    (2, 1, 129, 517, 128, 4),
+    (1, 1, 1, 1, 64, 1),
+    (1, 1, 1, 1, 128, 1),
+    (1, 3, 200, 777, 128, 7),
+    (1, 1, 257, 64, 64, 64),
+    (1, 2, 128, 2048, 128, 8),
+]
+
+
+def _bf16_forward_case(B, H, Nq, Nk, d, R, seed=11, std=1.0):
+    t, x = random_case(seed, B, H, Nq, Nk, d, store="bf16", std=std)
+    g = _dev(t, "bf16")
+    scale = float(np.float32(1 / math.sqrt(d)))
+    return t, x, g, scale
+
+
+@pytest.mark.parametrize("B,H,Nq,Nk,d,R", BF16_SHAPES)
+def test_bf16_forward(B, H, Nq, Nk, d, R):
+    t, x, g, scale = _bf16_forward_case(B, H, Nq, Nk, d, R)
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    po, pl = ringx.ringx_attn_fwd_partials(g["q"], g["k"], g["v"], R, scale=scale)
+    torch.cuda.synchronize()
+    ref_po, ref_pl = oracle.attention_partials(x["q"], x["k"], x["v"], scale, R)
+    ref_o, ref_l = oa.lse_merge(ref_po, ref_pl)
+    errs = dict(out=rel_rms_err(to_host_f64(out), ref_o), lse=max_abs_err(to_host_f64(lse), ref_l),
+                part_out=rel_rms_err(to_host_f64(po), ref_po),
+                part_lse=max_abs_err(to_host_f64(pl), ref_pl))
+    _report(f"bf16 fwd {(B, H, Nq, Nk, d, R)}", **errs)
+    assert errs["out"] <= TOL_BF16_REL_RMS and errs["part_out"] <= TOL_BF16_REL_RMS
+    assert errs["lse"] <= TOL_BF16_LSE and errs["part_lse"] <= TOL_BF16_LSE
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_bf16_fused_equals_partials_plus_merge(d):
+    B, H, Nq, Nk, R = 1, 2, 200, 1500, 5
+    t, x, g, scale = _bf16_forward_case(B, H, Nq, Nk, d, R, seed=12)
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    po, pl = ringx.ringx_attn_fwd_partials(g["q"], g["k"], g["v"], R, scale=scale)
+    mo, ml = ringx.ringx_lse_merge(po, pl, out_dtype=torch.bfloat16)
+    mo32, ml32 = ringx.ringx_lse_merge(po, pl, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oa.lse_merge(*oracle.attention_partials(x["q"], x["k"], x["v"], scale, R))
+    # the same partials, merged in the kernel's registers or by the standalone merge
+    assert rel_rms_err(to_host_f64(mo), to_host_f64(out)) <= 2 * 2.0 ** -8 * 8
+    assert max_abs_err(to_host_f64(ml), to_host_f64(lse)) <= 1e-5
+    assert max_abs_err(to_host_f64(ml32), to_host_f64(ml)) == 0.0
+    assert rel_rms_err(to_host_f64(mo32), ref_o) <= TOL_BF16_REL_RMS
+    # standalone merge of exact partials (fp32 in, fp32 out) is fp32-accurate
+    ref_po, ref_pl = oracle.attention_partials(x["q"], x["k"], x["v"], scale, R)
+    po_t = torch.from_numpy(ref_po.astype(np.float32)).cuda()
+    pl_t = torch.from_numpy(ref_pl.astype(np.float32)).cuda()
+    eo, el = ringx.ringx_lse_merge(po_t, pl_t, out_dtype=torch.float32)
+    ref_mo, ref_ml = oa.lse_merge(ref_po.astype(np.float32).astype(np.float64),
+                                  ref_pl.astype(np.float32).astype(np.float64))
+    assert max_abs_err(to_host_f64(eo), ref_mo) <= TOL_F32
+    assert max_abs_err(to_host_f64(el), ref_ml) <= TOL_F32
+
+
+def test_merge_ignores_minus_inf_partials():
+    R, B, H, Nq, d = 3, 1, 1, 10, 64
+    rng = np.random.default_rng(3)
+    po = rng.standard_normal((R, B, H, Nq, d)).astype(np.float32)
+    pl = rng.standard_normal((R, B, H, Nq)).astype(np.float32)
+    pl[1] = -np.inf
+    po[1] = 1e30
+    eo, el = ringx.ringx_lse_merge(torch.from_numpy(po).cuda(), torch.from_numpy(pl).cuda(),
+                                   out_dtype=torch.float32)
+    ro, rl = oa.lse_merge(po.astype(np.float64), pl.astype(np.float64))
+    assert max_abs_err(to_host_f64(eo), ro) <= TOL_F32
+    assert max_abs_err(to_host_f64(el), rl) <= TOL_F32
+
+
+def test_bf16_forward_independent_of_R():
+    B, H, Nq, Nk, d = 1, 2, 150, 3000, 128
+    t, x, g, scale = _bf16_forward_case(B, H, Nq, Nk, d, 1, seed=13)
+    o1, l1 = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], 1, scale=scale)
+    o8, l8 = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], 8, scale=scale)
+    torch.cuda.synchronize()
+    assert rel_rms_err(to_host_f64(o8), to_host_f64(o1)) <= TOL_BF16_REL_RMS
+    assert max_abs_err(to_host_f64(l8), to_host_f64(l1)) <= 1e-4
+
+
+def test_bf16_forward_determinism_and_q_permutation():
+    """Each query's arithmetic is independent of every other query: a permutation of the Q rows
+    permutes out and lse bit for bit, and repeated runs are bitwise identical."""
+    B, H, Nq, Nk, d, R = 1, 2, 256, 1200, 128, 3
+    t, x, g, scale = _bf16_forward_case(B, H, Nq, Nk, d, R, seed=14)
+    o1, l1 = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    o2, l2 = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    perm = torch.from_numpy(np.random.default_rng(5).permutation(Nq)).cuda()
+    qp = g["q"][:, :, perm].contiguous()
+    op, lp = ringx.ringx_attn_fwd(qp, g["k"], g["v"], R, scale=scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert torch.equal(op, o1[:, :, perm]) and torch.equal(lp, l1[:, :, perm])
+
+
+# Input scales of the paper-shaped workloads: d=64 inputs ~0.5 N(0,1) with dO ~ N(0,1) (the
+# single-shard 16k workload), d=128 inputs and dO ~ N(0,1)/sqrt(2) (the ring-share workloads).
+def _workload_std(d):
+    return (0.5, 1.0) if d == 64 else (2 ** -0.5, 2 ** -0.5)
+
+
+@pytest.mark.parametrize("B,H,Nq,Nk,d,R", [(1, 2, 300, 1000, 64, 3), (1, 2, 100, 700, 128, 4),
+                                           (2, 1, 65, 129, 128, 1), (1, 3, 257, 2000, 64, 5),
+                                           (1, 1, 37, 300, 128, 300)])
+def test_bf16_backward(B, H, Nq, Nk, d, R):
+    std, do_std = _workload_std(d)
+    t, x = random_case(21, B, H, Nq, Nk, d, store="bf16", std=std, do_std=do_std)
+    g = _dev(t, "bf16")
+    scale = float(np.float32(1 / math.sqrt(d)))
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    torch.cuda.synchronize()
+    ref_o, ref_l = oracle.attention(x["q"], x["k"], x["v"], scale)
+    rq, rk, rv = oracle.attention_bwd(x["q"], x["k"], x["v"], ref_o, x["do"], ref_l, scale)
+    errs = dict(dq=rel_rms_err(to_host_f64(dq), rq), dk=rel_rms_err(to_host_f64(dk), rk),
+                dv=rel_rms_err(to_host_f64(dv), rv))
+    _report(f"bf16 bwd {(B, H, Nq, Nk, d, R)}", **errs)
+    for k, e in errs.items():
+        assert e <= TOL_BF16_REL_RMS, (k, e)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_bf16_backward_single_key(d):
+    """Nk = 1: every P_ij is 1, so dQ = 0, dK = 0 and dV_0 = sum_i dO_i (closed forms; the exact
+    zeros have no RMS scale, so they are checked in absolute terms against O(1) inputs)."""
+    t, x = random_case(23, 1, 2, 77, 1, d, store="bf16", std=1.0)
+    g = _dev(t, "bf16")
+    scale = float(np.float32(1 / math.sqrt(d)))
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], 1, scale=scale)
+    dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, 1, scale=scale)
+    torch.cuda.synchronize()
+    assert float(torch.max(torch.abs(dq))) <= 1e-3
+    assert float(torch.max(torch.abs(dk))) <= 1e-3
+    assert rel_rms_err(to_host_f64(dv)[:, :, 0], x["do"].sum(axis=2)) <= TOL_BF16_REL_RMS
+
+
+def test_bf16_backward_accumulate_and_invariants():
+    B, H, Nq, Nk, d, R = 1, 2, 200, 600, 128, 3
+    t, x = random_case(22, B, H, Nq, Nk, d, store="bf16", std=1.0)
+    g = _dev(t, "bf16")
+    scale = float(np.float32(1 / math.sqrt(d)))
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    base_k = torch.randn_like(dk)
+    base_v = torch.randn_like(dv)
+    dk2, dv2 = base_k.clone(), base_v.clone()
+    ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale, dk=dk2,
+                         dv=dv2, accumulate_dkv=True)
+    torch.cuda.synchronize()
+    assert torch.allclose(dk2 - base_k, dk, rtol=0, atol=1e-5)
+    assert torch.allclose(dv2 - base_v, dv, rtol=0, atol=1e-5)
+    # dk and dv are written by plain stores: bitwise reproducible
+    _, dk3, dv3 = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    torch.cuda.synchronize()
+    assert torch.equal(dk3, dk) and torch.equal(dv3, dv)
+    # sum_j dV_j = sum_i dO_i and sum_j dK_j = 0, per (b, h)
+    sdv = dv.double().sum(dim=2)
+    sdo = g["do"].double().sum(dim=2)
+    assert torch.max(torch.abs(sdv - sdo)) <= 2e-2 * torch.max(torch.abs(dv.double()).sum(dim=2))
+    sdk = dk.double().sum(dim=2)
+    assert torch.max(torch.abs(sdk)) <= 2e-2 * torch.max(torch.abs(dk.double()).sum(dim=2))
+
+
+def test_errors_leave_outputs_untouched():
+    q = torch.randn((1, 1, 16, 64), device="cuda").to(torch.bfloat16)
+    k = torch.randn((1, 1, 8, 64), device="cuda").to(torch.bfloat16)
+    out = torch.full((1, 1, 16, 64), 7.0, device="cuda").to(torch.bfloat16)
+    lse = torch.full((1, 1, 16), 3.0, device="cuda")
+    with pytest.raises(ringx.RingxError):
+        ringx.ringx_attn_fwd(q, k, k.clone(), 9, out=out, lse=lse)    # R > Nk
+    with pytest.raises(ringx.RingxError):
+        ringx.ringx_attn_fwd(q, k, k.clone(), 1, scale=float("nan"), out=out, lse=lse)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0) and torch.all(lse == 3.0)
