@@ -1,0 +1,266 @@
+#!/usr/bin/env python3
+"""Throughput of ring-chunked attention (forward + recompute backward) on one MI355X.
+
+One step = one pass of the whole hot path over one batch of resident synthetic input:
+ringx_attn_fwd (every K/V chunk streamed, per-chunk local results merged by Eq. (5) in registers)
+followed by ringx_attn_bwd (preprocess D = rowsum(dO * O), then the recompute backward with dQ
+accumulated over every chunk).  The default workload is one GPU's share of an 8-way ring:
+B=1, H=16, d=128, a query shard of 32,768 tokens against all 262,144 keys (a 64^3 token grid) in
+R=8 chunks, bf16 storage, Q/K/V/dO ~ N(0,1)/sqrt(2).
+
+Throughput counts 12*B*H*Nq*Nk*d flops per step (4 in the forward's two contractions, 8 in the
+backward's four; the backward's recomputation of the scores is not credited).  Prints one JSON
+line on stdout; progress goes to stderr.
+
+    python bench.py [--gpus 1] [--steps 10] [--warmup 2] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "attention fwd+bwd TFLOP/s and % of bf16 MFMA peak at Nk=262,144, 1 GPU"
+PEAK_BF16_TFLOPS = 2516.6     # 256 CUs x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2507_16697_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload, src_hash):
+    """Measured HBM traffic of a kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE), if it was taken on
+    the kernel's current source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_hash") != src_hash:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(t, w, rows):
+    """The fp64 oracle on host cores: head 0, the first `rows` queries against all keys,
+    forward + backward.  Returns the baseline record (TFLOP/s of the same flop convention)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle
+    from paper_2507_16697_amd import inputs
+
+    q = inputs.to_f64(t["q"][0, 0, :rows], "bf16")
+    k = inputs.to_f64(t["k"][0, 0], "bf16")
+    v = inputs.to_f64(t["v"][0, 0], "bf16")
+    do = inputs.to_f64(t["do"][0, 0, :rows], "bf16")
+    t0 = time.perf_counter()
+    o, lse = oracle.head_attention(q, k, v, w.scale)
+    D = oracle.head_bwd_preprocess(o, do)
+    dq, dk, dv = oracle.head_attention_bwd(q, k, v, do, lse, D, w.scale)
+    sec = time.perf_counter() - t0
+    assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk))
+    flops = 12.0 * rows * w.Nk * w.d
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {
+        "value": flops / sec / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+        "seconds": sec,
+        "sample": f"fp64 oracle, head 0 of {w.name}: queries 0..{rows - 1} against all {w.Nk} "
+                  f"keys, forward + backward, {flops:.3e} flops (12*rows*Nk*d)",
+        "cpu": _cpu_model(),
+    }
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="ring8_nk262k_d128")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=256)
+    ap.add_argument("--no-merge", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's share of the ring; --gpus {args.gpus} is not supported "
+              "(this build has no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2507_16697_amd import inputs, ringx
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": src.numel() * 4, "bytes_written": dst.numel() * 4,
+                          "launches": 3}), flush=True)
+        return
+    w = inputs.WORKLOADS[args.workload]
+    if w.dtype != "bf16" or w.passes != "fwd+bwd":
+        print("bench.py times fwd+bwd bf16 workloads", file=sys.stderr)
+        sys.exit(2)
+    ringx.lib()  # fail loudly if the library is missing
+
+    log(f"[bench] generating {w.name} inputs (seeded, host)")
+    t0 = time.time()
+    t = inputs.make_workload(w.name)
+    log(f"[bench] inputs ready in {time.time() - t0:.1f}s; moving to HBM")
+    dev = torch.device("cuda:0")
+
+    def to_dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    q, k, v, do = (to_dev(t[n]) for n in ("q", "k", "v", "do"))
+    B, H, Nq, Nk, d, R = w.B, w.H, w.Nq, w.Nk, w.d, w.R
+    out = torch.empty_like(q)
+    lse = torch.empty((B, H, Nq), dtype=torch.float32, device=dev)
+    dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=dev)
+    dk = torch.empty((B, H, Nk, d), dtype=torch.float32, device=dev)
+    dv = torch.empty((B, H, Nk, d), dtype=torch.float32, device=dev)
+    ws = torch.empty(ringx.ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, ringx.RINGX_BF16),
+                     dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
+        ringx.ringx_attn_bwd(q, k, v, out, do, lse, R, scale=w.scale, dq=dq, dk=dk, dv=dv,
+                             workspace=ws, stream=stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup step {i + 1}/{args.warmup} done")
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for s in range(K):
+        ev[s][0].record(stream)
+        ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
+        ev[s][1].record(stream)
+        ringx.ringx_attn_bwd(q, k, v, out, do, lse, R, scale=w.scale, dq=dq, dk=dk, dv=dv,
+                             workspace=ws, stream=stream)
+        ev[s][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = ev[0][0].elapsed_time(ev[K - 1][2])
+    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
+    bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / K
+    ms_step = total_ms / K
+    log(f"[bench] timed {K} steps: {ms_step:.2f} ms/step (fwd {fwd_ms:.2f}, bwd {bwd_ms:.2f}; "
+        f"wall {wall * 1e3 / K:.2f})")
+    if not (torch.isfinite(out.float()).all() and torch.isfinite(dq).all()):
+        raise RuntimeError("non-finite results")
+
+    U = w.gemm_unit()                      # 2*B*H*Nq*Nk*d
+    value = 6 * U / (ms_step * 1e-3) / 1e12
+    fwd_tf = 2 * U / (fwd_ms * 1e-3) / 1e12
+    bwd_tf = 4 * U / (bwd_ms * 1e-3) / 1e12
+
+    fwd_hash = kernel_source_hash(["fwd_bf16.hip", "ringx_device.h"])
+    bwd_hash = kernel_source_hash(["bwd_bf16.hip", "ringx_device.h"])
+    kernels = {
+        "fwd_bf16": {"ms": fwd_ms, "flops": 2 * U, "tflops": fwd_tf, "frac": fwd_tf / PEAK_BF16_TFLOPS,
+                     "traffic": load_traffic("fwd_bf16", w.name, fwd_hash)},
+        "bwd_pre+bwd_bf16": {"ms": bwd_ms, "flops": 4 * U, "tflops": bwd_tf,
+                             "frac": bwd_tf / PEAK_BF16_TFLOPS,
+                             "traffic": load_traffic("bwd_bf16", w.name, bwd_hash)},
+    }
+    dominant = "bwd" if bwd_ms >= fwd_ms else "fwd"
+    dom = kernels["bwd_pre+bwd_bf16"] if dominant == "bwd" else kernels["fwd_bf16"]
+    roofline = {
+        "kernel": "bwd_bf16_kernel" if dominant == "bwd" else "fwd_bf16_kernel",
+        "bound": "mfma", "achieved": dom["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+        "frac": dom["frac"], "traffic": dom["traffic"],
+        "work_per_launch": f"{dom['flops']:.4e} flops ("
+                           + ("8*B*H*Nq*Nk*d: the backward's four contractions"
+                              if dominant == "bwd" else "4*B*H*Nq*Nk*d: the forward's two contractions")
+                           + ")",
+    }
+
+    # standalone Eq. (5) merge of the R per-chunk partials (an HBM-bound kernel)
+    if not args.no_merge:
+        part_out, part_lse = ringx.ringx_attn_fwd_partials(q, k, v, R, scale=w.scale, stream=stream)
+        mo = torch.empty_like(q)
+        ml = torch.empty_like(lse)
+        ringx.ringx_lse_merge(part_out, part_lse, out=mo, lse=ml, stream=stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nm = 10
+        e0.record(stream)
+        for _ in range(nm):
+            ringx.ringx_lse_merge(part_out, part_lse, out=mo, lse=ml, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        mms = e0.elapsed_time(e1) / nm
+        rows = B * H * Nq
+        mbytes = R * rows * (4 * d + 4) + rows * (2 * d + 4)
+        kernels["lse_merge"] = {"ms": mms, "bytes": mbytes, "GB/s": mbytes / (mms * 1e-3) / 1e9,
+                                "frac": mbytes / (mms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+                                "traffic": load_traffic("lse_merge", w.name,
+                                                        kernel_source_hash(["merge.hip", "ringx_device.h"]))}
+        log(f"[bench] lse_merge {mms:.3f} ms, {kernels['lse_merge']['GB/s']:.0f} GB/s")
+        del part_out, part_lse
+
+    result = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "H": H, "Nq": Nq, "Nk": Nk, "d": d, "R": R,
+                   "flops_per_step": 6 * U, "flop_convention": "12*B*H*Nq*Nk*d per fwd+bwd step",
+                   "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
+                   "tflops_fa_convention_14": 7 * U / (ms_step * 1e-3) / 1e12},
+        "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "roofline": roofline,
+        "kernels": kernels,
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline: oracle on {args.cpu_rows} query rows of head 0")
+        result["cpu_baseline"] = cpu_baseline(t, w, args.cpu_rows)
+        log(f"[bench] cpu baseline {result['cpu_baseline']['seconds']:.1f}s")
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -4,9 +4,9 @@ This module generates inputs only: it holds none of the attention arithmetic, an
 piece of code shared by the HIP path's tests/benchmark and by the fp64 oracle.
 
 Rules common to every workload:
-  * numpy.random.default_rng(seed) (PCG64);
-  * tensors are drawn in the order Q, K, V, dO, each as per-(b, h) slabs rng.standard_normal((N, d))
-    in C order (so a huge tensor streams slab by slab and the stream is defined slab by slab);
+  * every (tensor, b, h) slab is its own PCG64 stream,
+    numpy.random.default_rng([seed, tensor, b, h]).standard_normal((N, d)), with tensor = 0, 1, 2, 3
+    for Q, K, V, dO (independent streams, so a huge tensor is generated slab by slab, in parallel);
   * values are scaled in fp64, then stored as fp32 (round to nearest even) or as bf16 bits
     (fp64 -> fp32 -> bf16, each step round to nearest even).
 
@@ -14,8 +14,8 @@ Workloads (layout [B, H, N, d]):
   exact_fp32_n1k         B=1 H=2  Nq=Nk=1024     d=64  R=4 fp32  seed 0 ~N(0,1)          fwd
   shard_n16k_d64         B=1 H=16 Nq=Nk=16384    d=64  R=4 bf16  seed 1 ~0.5 N(0,1); dO seed 2 ~N(0,1)
                          (tokens of a 32x32x16 patch grid, x fastest; the values are i.i.d.)
-  ring8_nk262k_d128      B=1 H=16 Nq=32768 Nk=262144 d=128 R=8 bf16 seed 3 ~N(0,1)/sqrt2, dO continues
-                         seed 3 (one GPU's query shard of an 8-way ring over a 64^3 token grid)
+  ring8_nk262k_d128      B=1 H=16 Nq=32768 Nk=262144 d=128 R=8 bf16 seed 3 ~N(0,1)/sqrt2, dO seed 3
+                         too (one GPU's query shard of an 8-way ring over a 64^3 token grid)
   turbulence_nk262k_d64  B=1 H=16 Nq=65536 Nk=262144 d=64 R=4 bf16, tokens of a synthetic
                          divergence-free k^-5/3 velocity field (see turbulence_qkv); fwd only
   long_nk524k_d128       B=1 H=16 Nq=65536 Nk=524288 d=128 R=8 bf16 seed 5, Q,K,V,dO ~N(0,1)/sqrt2
@@ -26,6 +26,7 @@ Turbulence tokens stand in for the JHTDB forced-isotropic-turbulence snapshots t
 
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import hashlib
 import math
@@ -45,10 +46,11 @@ def f64_to_f32(x) -> np.ndarray:
 def f32_to_bf16_bits(x32) -> np.ndarray:
     """fp32 -> bf16 bit pattern (uint16), round to nearest even on the 16 dropped bits.
 
-    Inputs here are finite; NaN payloads are not handled.
+    Inputs here are finite (for finite values the 32-bit sum below cannot overflow); NaN payloads
+    are not handled.
     """
-    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    rounded = (u + np.uint64(0x7FFF) + ((u >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)
+    u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return rounded.astype(np.uint16)
 
 
@@ -86,7 +88,7 @@ class Workload:
     passes: str         # "fwd" or "fwd+bwd"
     seed: int
     std: float          # Q, K, V ~ std * N(0, 1)
-    do_seed: int | None  # None: dO continues the Q/K/V generator
+    do_seed: int | None  # None: dO uses the Q/K/V seed
     do_std: float
     kind: str = "iid"   # "iid" or "turbulence"
 
@@ -115,34 +117,43 @@ WORKLOADS = {
 }
 
 
-def _draw_slabs(rng, B, H, N, d, std, store) -> np.ndarray:
-    """Per-(b, h) slabs of std * N(0,1) in C order, converted slab by slab to the storage type."""
-    if store == "fp32":
-        out = np.empty((B, H, N, d), dtype=np.float32)
+_TENSOR_ID = {"q": 0, "k": 1, "v": 2, "do": 3}
+
+
+def slab(seed: int, tensor: str, b: int, h: int, N: int, d: int, std: float, store: str):
+    """One (b, h) slab of `tensor`: std * N(0,1) from default_rng([seed, tensor id, b, h])."""
+    x = np.random.default_rng([seed, _TENSOR_ID[tensor], b, h]).standard_normal((N, d)) * std
+    return f64_to_f32(x) if store == "fp32" else f64_to_bf16_bits(x)
+
+
+def _draw(seed, tensor, B, H, N, d, std, store, threads) -> np.ndarray:
+    out = np.empty((B, H, N, d), dtype=np.float32 if store == "fp32" else np.uint16)
+
+    def fill(bh):
+        b, h = divmod(bh, H)
+        out[b, h] = slab(seed, tensor, b, h, N, d, std, store)
+
+    if threads <= 1 or B * H == 1:
+        for bh in range(B * H):
+            fill(bh)
     else:
-        out = np.empty((B, H, N, d), dtype=np.uint16)
-    for b in range(B):
-        for h in range(H):
-            slab = rng.standard_normal((N, d)) * std
-            out[b, h] = f64_to_f32(slab) if store == "fp32" else f64_to_bf16_bits(slab)
+        with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+            list(ex.map(fill, range(B * H)))
     return out
 
 
 def make_iid(B, H, Nq, Nk, d, *, seed, std=1.0, store="bf16", with_do=True, do_seed=None,
-             do_std=1.0) -> dict:
+             do_std=1.0, threads=None) -> dict:
     """i.i.d. Gaussian Q, K, V (and dO) with the common drawing rules.
 
     Returns {"q","k","v"[,"do"]}: float32 arrays for store="fp32", uint16 bf16 bits for "bf16".
     """
-    rng = np.random.default_rng(seed)
-    t = {
-        "q": _draw_slabs(rng, B, H, Nq, d, std, store),
-        "k": _draw_slabs(rng, B, H, Nk, d, std, store),
-        "v": _draw_slabs(rng, B, H, Nk, d, std, store),
-    }
+    threads = threads or min(16, os.cpu_count() or 1)
+    t = {name: _draw(seed, name, B, H, n, d, std, store, threads)
+         for name, n in (("q", Nq), ("k", Nk), ("v", Nk))}
     if with_do:
-        rng_do = rng if do_seed is None else np.random.default_rng(do_seed)
-        t["do"] = _draw_slabs(rng_do, B, H, Nq, d, do_std, store)
+        t["do"] = _draw(seed if do_seed is None else do_seed, "do", B, H, Nq, d, do_std, store,
+                        threads)
     return t
 
 

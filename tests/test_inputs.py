@@ -36,21 +36,24 @@ def test_seeded_draws_are_deterministic():
     assert inputs.sha256_of(a["q"]) != inputs.sha256_of(c["q"])
 
 
-def test_slab_draws_equal_one_shot_draws():
+def test_each_slab_is_its_own_stream():
     B, H, nq, nk, d = 2, 3, 5, 7, 4
-    t = inputs.make_iid(B, H, nq, nk, d, seed=3, std=1.0, store="fp32")
-    rng = np.random.default_rng(3)
-    q = rng.standard_normal((B, H, nq, d))
-    k = rng.standard_normal((B, H, nk, d))
-    v = rng.standard_normal((B, H, nk, d))
-    do = rng.standard_normal((B, H, nq, d))
-    for key, ref in (("q", q), ("k", k), ("v", v), ("do", do)):
-        np.testing.assert_array_equal(t[key], ref.astype(np.float32))
+    t = inputs.make_iid(B, H, nq, nk, d, seed=3, std=0.5, do_std=0.5, store="fp32", threads=4)
+    for name, n, tid in (("q", nq, 0), ("k", nk, 1), ("v", nk, 2), ("do", nq, 3)):
+        for b in range(B):
+            for h in range(H):
+                ref = np.random.default_rng([3, tid, b, h]).standard_normal((n, d)) * 0.5
+                np.testing.assert_array_equal(t[name][b, h], ref.astype(np.float32))
+    assert not np.array_equal(t["q"][0, 0], t["q"][0, 1])
+    serial = inputs.make_iid(B, H, nq, nk, d, seed=3, std=0.5, store="bf16", threads=1)
+    parallel = inputs.make_iid(B, H, nq, nk, d, seed=3, std=0.5, store="bf16", threads=5)
+    for name in serial:
+        np.testing.assert_array_equal(serial[name], parallel[name])
 
 
 def test_separate_do_seed():
     t = inputs.make_iid(1, 1, 4, 6, 2, seed=1, std=0.5, store="fp32", do_seed=2, do_std=1.0)
-    ref = np.random.default_rng(2).standard_normal((4, 2)).astype(np.float32)
+    ref = np.random.default_rng([2, 3, 0, 0]).standard_normal((4, 2)).astype(np.float32)
     np.testing.assert_array_equal(t["do"][0, 0], ref)
 
 
