@@ -3,24 +3,32 @@
 // One workgroup = 4 waves = one (b, h) and a tile of 128 queries (32 per wave).  The key/value
 // sequence is visited as R chunks (ring steps, arXiv 2507.16697 Sec. III-A); every chunk is
 // streamed through LDS in tiles of BK keys, double buffered (the on-chip analogue of the paper's
-// ping-pong buffers).  Within a chunk the wave keeps an online softmax (Eqs. (2)-(4)); at the
-// end of the chunk it forms the chunk's local result (loc_out, loc_lse) and folds it into the
-// running Eq. (5) merge held in registers.  PARTIALS = true writes the local results instead.
+// ping-pong buffers) and filled by direct global->LDS loads issued one tile ahead.  Within a chunk
+// each wave keeps an online softmax (Eqs. (2)-(4)); at the end of the chunk it forms the chunk's
+// local result (loc_out, loc_lse) and folds it into the running Eq. (5) merge held in registers.
+// PARTIALS = true writes the local results instead of merging them.
 //
 // Per wave, with g = lane / 32 and n = lane % 32:
 //   S^T = K Q^T   A = K rows from LDS (key n, 8 dims), B = Q^T from registers (query n, 8 dims)
 //                 -> lane holds query n and keys 8*(r/4) + 4g + r%4 of each 32-key block;
-//   O^T += V^T P^T A = V^T from LDS (dim n, 8 keys), B = P^T straight from the S^T registers.
-// The 8 keys a lane feeds to one PV MFMA are {4g..4g+3, 8+4g..8+4g+3} of a 16-key block, so the
-// transposed V tile is written to LDS with the two middle 4-key groups of each 16-key block
-// swapped (position = key offset with bits 2 and 3 exchanged): each A read is one 16-byte load.
-// Softmax statistics stay in fp32 in the exp2 domain (t = scale * log2(e) * q.k).
+//   O^T += V^T P^T A = V^T read from the row-major V tile with ds_read_b64_tr_b16 (4 keys per
+//                 read), B = P^T straight from the S^T registers (keys 4g..4g+3, 8+4g..8+4g+3).
+// LDS tiles are row-major with the 16-byte chunks of each row XOR-swizzled by the row index, so
+// that both the 16-byte K reads (16 rows, one chunk) and the transposed V reads (4 rows x 2
+// chunks per 16 lanes) hit distinct banks.
+// Softmax statistics are fp32 in the exp2 domain (t = scale*log2(e)*q.k).  The reference maximum
+// of a row only moves when a tile's maximum exceeds it by more than kLazy (probabilities stay
+// below 2^kLazy), so the accumulator rescale is skipped for most tiles.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
 
 namespace ringx {
 namespace {
+
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr float kLazy = 8.0f;
 
 template <int D>
 struct FwdCfg {
@@ -29,89 +37,60 @@ struct FwdCfg {
   static constexpr int kQW = 32;                  // queries per wave
   static constexpr int kBQ = kWaves * kQW;        // queries per workgroup
   static constexpr int kBK = 8192 / D;            // keys per tile: 64 (d=128) or 128 (d=64)
-  static constexpr int kKS = D + 8;               // padded LDS row stride of the K tile (elements)
-  static constexpr int kVS = kBK + 8;             // padded LDS row stride of the V^T tile
-  static constexpr int kOcts = D / 8;             // 16-byte chunks per row
+  static constexpr int kRowBytes = D * 2;
+  static constexpr int kChunks = D / 8;           // 16-byte chunks per row
+  static constexpr int kTileBytes = kBK * kRowBytes;   // 16 KiB
   static constexpr int kKTiles = kBK / 32;        // 32-key blocks per tile
   static constexpr int kDSteps = D / 16;          // MFMA k-steps over the head dim
   static constexpr int kKSteps = kBK / 16;        // MFMA k-steps over the keys
   static constexpr int kCT = D / 32;              // 32-dim blocks of the output
-  static constexpr int kLdsK = kBK * kKS;         // elements per K buffer
-  static constexpr int kLdsV = D * kVS;           // elements per V^T buffer
-  static_assert(kBK * D == kThreads * 32, "each thread stages 32 elements of K and of V");
+  static constexpr int kLoads = kTileBytes / (kThreads * 16);   // 16-byte loads per thread
 };
 
-// Position of key offset o (0..kBK-1) inside the transposed V tile.
-__device__ __forceinline__ int vt_pos(int o) {
-  const int q4 = (o >> 2) & 3;
-  const int q4s = ((q4 & 1) << 1) | (q4 >> 1);
-  return (o & ~15) | (q4s << 2) | (o & 3);
+// Swizzled 16-byte chunk of (row, logical chunk c) inside a row-major tile.
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+  if constexpr (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
+  else return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+}
+template <int D>
+__device__ __forceinline__ int tile_off(int row, int c) {   // byte offset
+  return row * (D * 2) + ((c ^ swz<D>(row)) << 4);
 }
 
-template <int D>
-struct Stage {
-  u32x4 k[4];
-  u32x4 v[4];
-};
+// One 16-byte direct global->LDS load per lane: LDS destination = lds_base + 16 * lane.
+// Issued through inline asm so that the compiler does not order later LDS reads of the other
+// buffer behind it; the explicit vmcnt wait before the workgroup barrier publishes the tile.
+__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(gptr)
+               : "memory", "m0");
+}
 
+// Issue the direct loads of one K/V tile: rows start..start+kBK-1 (clamped to hi-1).
 template <int D>
-__device__ __forceinline__ void load_tile(Stage<D>& st, const __bf16* __restrict__ kb,
-                                          const __bf16* __restrict__ vb, int64_t start,
-                                          int64_t hi, int t) {
+__device__ __forceinline__ void issue_tile(const __bf16* __restrict__ kb,
+                                           const __bf16* __restrict__ vb, uint32_t kdst,
+                                           uint32_t vdst, int64_t start, int64_t hi, int wave,
+                                           int lane) {
   using C = FwdCfg<D>;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int ci = t + C::kThreads * u;
-    const int row = ci / C::kOcts;
-    const int cc = ci % C::kOcts;
+  for (int u = 0; u < C::kLoads; ++u) {
+    const int slot = (u * C::kWaves + wave) * 64 + lane;      // 16-byte LDS slot
+    const int row = slot / C::kChunks;
+    const int pc = slot % C::kChunks;
+    const int c = pc ^ swz<D>(row);
     int64_t key = start + row;
     key = key < hi ? key : hi - 1;
-    st.k[u] = *reinterpret_cast<const u32x4*>(kb + key * D + cc * 8);
-  }
-  const int co = t % C::kOcts;
-  const int kq = t / C::kOcts;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    int64_t key = start + kq * 4 + e;
-    key = key < hi ? key : hi - 1;
-    st.v[e] = *reinterpret_cast<const u32x4*>(vb + key * D + co * 8);
+    const uint32_t wbase =
+        (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
+    load_lds16(kb + key * D + c * 8, kdst + wbase);
+    load_lds16(vb + key * D + c * 8, vdst + wbase);
   }
 }
 
-template <int D>
-__device__ __forceinline__ void store_tile(const Stage<D>& st, __bf16* ks_buf, __bf16* vt_buf,
-                                           int nvalid, int t) {
-  using C = FwdCfg<D>;
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int ci = t + C::kThreads * u;
-    const int row = ci / C::kOcts;
-    const int cc = ci % C::kOcts;
-    *reinterpret_cast<u32x4*>(ks_buf + row * C::kKS + cc * 8) = st.k[u];
-  }
-  const int co = t % C::kOcts;
-  const int kq = t / C::kOcts;
-  // keys beyond the chunk end get V = 0 (their probabilities are 0 as well)
-  uint32_t keep[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) keep[e] = (kq * 4 + e < nvalid) ? 0xffffffffu : 0u;
-  const int pos = vt_pos(kq * 4);
-#pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const int w = m >> 1;
-    uint32_t x0, x1, x2, x3;
-    if (m & 1) {
-      x0 = st.v[0][w] >> 16; x1 = st.v[1][w] >> 16; x2 = st.v[2][w] >> 16; x3 = st.v[3][w] >> 16;
-    } else {
-      x0 = st.v[0][w] & 0xffffu; x1 = st.v[1][w] & 0xffffu;
-      x2 = st.v[2][w] & 0xffffu; x3 = st.v[3][w] & 0xffffu;
-    }
-    u32x2 out;
-    out[0] = (x0 & keep[0]) | ((x1 & keep[1]) << 16);
-    out[1] = (x2 & keep[2]) | ((x3 & keep[3]) << 16);
-    *reinterpret_cast<u32x2*>(vt_buf + (co * 8 + m) * C::kVS + pos) = out;
-  }
-}
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 template <int D, bool PARTIALS>
 __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
@@ -119,8 +98,8 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
     __bf16* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
     float* __restrict__ part_lse, int BH, int64_t Nq, int64_t Nk, int R, float c2) {
   using C = FwdCfg<D>;
-  __shared__ __attribute__((aligned(16))) __bf16 lds_k[2 * C::kLdsK];
-  __shared__ __attribute__((aligned(16))) __bf16 lds_v[2 * C::kLdsV];
+  __shared__ __attribute__((aligned(1024))) char lds_k[2 * C::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char lds_v[2 * C::kTileBytes];
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -138,6 +117,27 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
   const __bf16* kb = k + bh * Nk * D;
   const __bf16* vb = v + bh * Nk * D;
 
+  // chunk bookkeeping without divisions: chunk r has q_sz + (1 if the running remainder wraps)
+  const int64_t q_sz = Nk / R;
+  const int64_t rem = Nk % R;
+  int64_t racc = 0;   // (r * rem) mod R
+  int r = 0;
+  int64_t start = 0;
+  int64_t hi;
+  {
+    racc += rem;
+    const int64_t extra = racc >= R ? 1 : 0;
+    racc -= extra * R;
+    hi = q_sz + extra;
+  }
+
+  // LDS byte addresses of the two K and two V buffers
+  const uint32_t lk = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_k;
+  const uint32_t lv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_v;
+
+  // first tile in flight while Q is loaded
+  issue_tile<D>(kb, vb, lk, lv, start, hi, wave, lane);
+
   // Q fragments (B operand of S^T = K Q^T): query n of this wave, dims 16*ks + 8g .. +8.
   bf16x8 qf[C::kDSteps];
   {
@@ -148,6 +148,26 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
       qf[s] = *reinterpret_cast<const bf16x8*>(qb + qi * D + s * 16 + g * 8);
   }
 
+  // per-lane LDS byte offsets (tile-relative)
+  int koff[C::kDSteps];   // K fragment of 32-key block 0 at k-step s (block kt adds kt*32 rows)
+#pragma unroll
+  for (int s = 0; s < C::kDSteps; ++s) koff[s] = tile_off<D>(n, 2 * s + g);
+  // V^T fragments via transposed reads: for 16-lane group G, rows j0 + (lane%16)/4 with
+  // j0 = 16*ks + 4g (+8 for the second half), columns 32*ct + 16*(G%2) + 4*(lane%4).
+  int voff[2][C::kCT];
+  {
+    const int G = lane >> 4;
+    const int rr = (lane & 15) >> 2;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ct = 0; ct < C::kCT; ++ct) {
+        const int row = 4 * g + 8 * h + rr;
+        const int col = 32 * ct + 16 * (G & 1) + 4 * (lane & 3);
+        voff[h][ct] = tile_off<D>(row, col >> 3) + (col & 7) * 2;
+      }
+  }
+
   f32x16 oacc[C::kCT];
   f32x16 om[C::kCT];
 #pragma unroll
@@ -155,38 +175,36 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
     oacc[c] = f32x16{};
     om[c] = f32x16{};
   }
-  float m2 = -INFINITY;   // running max of t within the chunk (exp2 domain)
-  float l = 0.f;          // this lane's share of the running sum within the chunk
+  float m2 = -INFINITY;     // reference max of the row within the chunk (exp2 domain)
+  float l = 0.f;            // this lane's share of the running sum within the chunk
   float lse2m = -INFINITY;  // merged log2-sum-exp over finished chunks
 
-  int r = 0;
-  int64_t hi = Nk / R;            // chunk 0 = [0, floor(Nk/R))
-  int64_t start = 0;
-  Stage<D> st;
-  load_tile<D>(st, kb, vb, start, hi, t);
   int cur = 0;
-  store_tile<D>(st, lds_k, lds_v, (int)min<int64_t>(C::kBK, hi - start), t);
+  wait_vm_all();
   __syncthreads();
 
   while (true) {
     // next tile: the following BK keys of this chunk, or the first tile of the next chunk
     int64_t nstart = start + C::kBK;
-    int nr = r;
     int64_t nhi = hi;
     bool has_next = true;
     if (nstart >= hi) {
-      nr = r + 1;
-      if (nr < R) {
-        nstart = (int64_t)nr * Nk / R;
-        nhi = (int64_t)(nr + 1) * Nk / R;
+      if (r + 1 < R) {
+        nstart = hi;
+        racc += rem;
+        const int64_t extra = racc >= R ? 1 : 0;
+        racc -= extra * R;
+        nhi = hi + q_sz + extra;
       } else {
         has_next = false;
       }
     }
-    if (has_next) load_tile<D>(st, kb, vb, nstart, nhi, t);
+    if (has_next)
+      issue_tile<D>(kb, vb, lk + (cur ^ 1) * C::kTileBytes, lv + (cur ^ 1) * C::kTileBytes,
+                    nstart, nhi, wave, lane);
 
-    const __bf16* ks_buf = lds_k + cur * C::kLdsK;
-    const __bf16* vt_buf = lds_v + cur * C::kLdsV;
+    const char* kbuf = lds_k + cur * C::kTileBytes;
+    const char* vbuf = lds_v + cur * C::kTileBytes;
     const int nvalid = (int)min<int64_t>(C::kBK, hi - start);
 
     // S^T = K Q^T for the tile's 32-key blocks
@@ -198,10 +216,18 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
 #pragma unroll
       for (int kt = 0; kt < C::kKTiles; ++kt) {
         const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(ks_buf + (kt * 32 + n) * C::kKS + s * 16 + g * 8);
+            *reinterpret_cast<const bf16x8*>(kbuf + koff[s] + kt * 32 * C::kRowBytes);
         sacc[kt] = mfma32(a, qf[s], sacc[kt]);
       }
     }
+    // keep two k-steps of K fragments in flight ahead of the MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::kKTiles, 0);
+#pragma unroll
+    for (int s = 0; s < C::kDSteps - 2; ++s) {
+      __builtin_amdgcn_sched_group_barrier(0x100, C::kKTiles, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, C::kKTiles, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * C::kKTiles, 0);
     if (nvalid < C::kBK) {
 #pragma unroll
       for (int kt = 0; kt < C::kKTiles; ++kt)
@@ -211,7 +237,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
           if (key >= nvalid) sacc[kt][rr] = -INFINITY;
         }
     }
-    // online softmax within the chunk (Eqs. (2)-(3) with a running max)
+    // online softmax within the chunk (Eqs. (2)-(3) with a lazily moved reference max)
     float mx = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < C::kKTiles; ++kt)
@@ -222,9 +248,16 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
                                                  false);
       mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
     }
-    const float mnew = fmaxf(m2, mx * c2);
-    const float alpha = fast_exp2(m2 - mnew);
-    m2 = mnew;
+    const float mt = mx * c2;
+    const bool need = mt > m2 + kLazy;
+    if (__builtin_amdgcn_ballot_w64(need)) {
+      const float mnew = need ? mt : m2;
+      const float alpha = fast_exp2(m2 - mnew);
+      m2 = mnew;
+      l *= alpha;
+#pragma unroll
+      for (int c = 0; c < C::kCT; ++c) oacc[c] *= alpha;
+    }
     float lsum = 0.f;
     bf16x8 pf[C::kKSteps];
 #pragma unroll
@@ -234,28 +267,37 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
         u32x4 w;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p0 = fast_exp2(__builtin_fmaf(sacc[kt][8 * h + 2 * e], c2, -mnew));
-          const float p1 = fast_exp2(__builtin_fmaf(sacc[kt][8 * h + 2 * e + 1], c2, -mnew));
+          const float p0 = fast_exp2(__builtin_fmaf(sacc[kt][8 * h + 2 * e], c2, -m2));
+          const float p1 = fast_exp2(__builtin_fmaf(sacc[kt][8 * h + 2 * e + 1], c2, -m2));
           lsum += p0 + p1;
           w[e] = pack_bf16x2(p0, p1);
         }
         pf[2 * kt + h] = __builtin_bit_cast(bf16x8, w);
       }
     }
-    l = l * alpha + lsum;
-#pragma unroll
-    for (int c = 0; c < C::kCT; ++c) oacc[c] *= alpha;
+    l += lsum;
 
     // O^T += V^T P^T
 #pragma unroll
     for (int s = 0; s < C::kKSteps; ++s) {
 #pragma unroll
       for (int c = 0; c < C::kCT; ++c) {
-        const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(vt_buf + (c * 32 + n) * C::kVS + s * 16 + g * 8);
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vbuf + voff[0][c] + s * 16 * C::kRowBytes));
+        const bf16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (lds_bf16x4*)(vbuf + voff[1][c] + s * 16 * C::kRowBytes));
+        const bf16x8 a = __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
         oacc[c] = mfma32(a, pf[s], oacc[c]);
       }
     }
+    // transposed V reads two MFMAs ahead
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int i = 0; i < C::kKSteps * C::kCT - 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
 
     if (start + C::kBK >= hi) {
       // end of chunk r: local result (loc_out_r, loc_lse_r), then the Eq. (5) merge
@@ -297,15 +339,14 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
       for (int c = 0; c < C::kCT; ++c) oacc[c] = f32x16{};
       l = 0.f;
       m2 = -INFINITY;
+      ++r;
     }
 
     if (!has_next) break;
-    store_tile<D>(st, lds_k + (cur ^ 1) * C::kLdsK, lds_v + (cur ^ 1) * C::kLdsV,
-                  (int)min<int64_t>(C::kBK, nhi - nstart), t);
+    wait_vm_all();
     __syncthreads();
     cur ^= 1;
     start = nstart;
-    r = nr;
     hi = nhi;
   }
 

@@ -211,13 +211,16 @@ def test_merge_ignores_minus_inf_partials():
 
 
 def test_bf16_forward_independent_of_R():
+    """The chunk count changes only the rounding: R = 1 and R = 8 both meet the oracle bar (two
+    bf16 outputs may differ by one bf16 ulp from each other, so they are not compared directly)."""
     B, H, Nq, Nk, d = 1, 2, 150, 3000, 128
-    t, x, g, scale = _bf16_forward_case(B, H, Nq, Nk, d, 1, seed=13)
-    o1, l1 = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], 1, scale=scale)
-    o8, l8 = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], 8, scale=scale)
-    torch.cuda.synchronize()
-    assert rel_rms_err(to_host_f64(o8), to_host_f64(o1)) <= TOL_BF16_REL_RMS
-    assert max_abs_err(to_host_f64(l8), to_host_f64(l1)) <= 1e-4
+    t, x, g, scale = _bf16_forward_case(B, H, Nq, Nk, d, 1, seed=13, std=2 ** -0.5)
+    ref_o, ref_l = oracle.attention(x["q"], x["k"], x["v"], scale)
+    for R in (1, 2, 8, 3000):
+        o, l = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+        torch.cuda.synchronize()
+        assert rel_rms_err(to_host_f64(o), ref_o) <= TOL_BF16_REL_RMS, R
+        assert max_abs_err(to_host_f64(l), ref_l) <= 1e-4, R
 
 
 def test_bf16_forward_determinism_and_q_permutation():
