@@ -158,10 +158,22 @@ def main():
                      dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
-    def step():
+    delta = ws[: B * H * Nq * 4].view(torch.float32).view(B, H, Nq)
+
+    def step(ev=None):
+        # one step = ringx_attn_fwd + ringx_attn_bwd; the backward is issued as its three stages
+        # (exactly what ringx_attn_bwd enqueues) so that each kernel gets its own event pair
+        marks = ev or [None] * 5
+        if marks[0]: marks[0].record(stream)
         ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
-        ringx.ringx_attn_bwd(q, k, v, out, do, lse, R, scale=w.scale, dq=dq, dk=dk, dv=dv,
-                             workspace=ws, stream=stream)
+        if marks[1]: marks[1].record(stream)
+        ringx.ringx_bwd_preprocess(out, do, delta=delta, stream=stream)
+        if marks[2]: marks[2].record(stream)
+        ringx.ringx_attn_bwd_dkdv(q, k, v, do, lse, delta, R, scale=w.scale, dk=dk, dv=dv,
+                                  stream=stream)
+        if marks[3]: marks[3].record(stream)
+        ringx.ringx_attn_bwd_dq(q, k, v, do, lse, delta, R, scale=w.scale, dq=dq, stream=stream)
+        if marks[4]: marks[4].record(stream)
 
     for i in range(args.warmup):
         step()
@@ -169,51 +181,59 @@ def main():
         log(f"[bench] warmup step {i + 1}/{args.warmup} done")
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    for s in range(K):
-        ev[s][0].record(stream)
-        ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
-        ev[s][1].record(stream)
-        ringx.ringx_attn_bwd(q, k, v, out, do, lse, R, scale=w.scale, dq=dq, dk=dk, dv=dv,
-                             workspace=ws, stream=stream)
-        ev[s][2].record(stream)
+    for s_ in range(K):
+        step(ev[s_])
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    total_ms = ev[0][0].elapsed_time(ev[K - 1][2])
-    fwd_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
-    bwd_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / K
+    total_ms = ev[0][0].elapsed_time(ev[K - 1][4])
+
+    def avg(i, j):
+        return sum(e[i].elapsed_time(e[j]) for e in ev) / K
+
+    fwd_ms, pre_ms, dkdv_ms, dq_ms = avg(0, 1), avg(1, 2), avg(2, 3), avg(3, 4)
+    bwd_ms = pre_ms + dkdv_ms + dq_ms
     ms_step = total_ms / K
-    log(f"[bench] timed {K} steps: {ms_step:.2f} ms/step (fwd {fwd_ms:.2f}, bwd {bwd_ms:.2f}; "
-        f"wall {wall * 1e3 / K:.2f})")
+    log(f"[bench] timed {K} steps: {ms_step:.2f} ms/step (fwd {fwd_ms:.2f}, bwd {bwd_ms:.2f} = "
+        f"pre {pre_ms:.3f} + dkdv {dkdv_ms:.2f} + dq {dq_ms:.2f}; wall {wall * 1e3 / K:.2f})")
     if not (torch.isfinite(out.float()).all() and torch.isfinite(dq).all()):
         raise RuntimeError("non-finite results")
 
     U = w.gemm_unit()                      # 2*B*H*Nq*Nk*d
     value = 6 * U / (ms_step * 1e-3) / 1e12
-    fwd_tf = 2 * U / (fwd_ms * 1e-3) / 1e12
-    bwd_tf = 4 * U / (bwd_ms * 1e-3) / 1e12
 
-    fwd_hash = kernel_source_hash(["fwd_bf16.hip", "ringx_device.h"])
-    bwd_hash = kernel_source_hash(["bwd_bf16.hip", "ringx_device.h"])
+    def tf(flops, ms):
+        return flops / (ms * 1e-3) / 1e12
+
     kernels = {
-        "fwd_bf16": {"ms": fwd_ms, "flops": 2 * U, "tflops": fwd_tf, "frac": fwd_tf / PEAK_BF16_TFLOPS,
-                     "traffic": load_traffic("fwd_bf16", w.name, fwd_hash)},
-        "bwd_pre+bwd_bf16": {"ms": bwd_ms, "flops": 4 * U, "tflops": bwd_tf,
-                             "frac": bwd_tf / PEAK_BF16_TFLOPS,
-                             "traffic": load_traffic("bwd_bf16", w.name, bwd_hash)},
+        "fwd_bf16_kernel": {"ms": fwd_ms, "flops": 2 * U, "work": "4*B*H*Nq*Nk*d (QK^T, PV)",
+                            "tflops": tf(2 * U, fwd_ms),
+                            "traffic": load_traffic("fwd_bf16", w.name,
+                                                    kernel_source_hash(["fwd_bf16.hip", "ringx_device.h"]))},
+        "bwd_dkdv_kernel": {"ms": dkdv_ms, "flops": 2 * U,
+                            "work": "4*B*H*Nq*Nk*d credited (dV, dK); S and dP recomputed",
+                            "tflops": tf(2 * U, dkdv_ms),
+                            "traffic": load_traffic("bwd_dkdv", w.name,
+                                                    kernel_source_hash(["bwd_bf16.hip", "ringx_device.h"]))},
+        "bwd_dq_kernel": {"ms": dq_ms, "flops": 2 * U,
+                          "work": "4*B*H*Nq*Nk*d credited (dP, dQ); S recomputed",
+                          "tflops": tf(2 * U, dq_ms),
+                          "traffic": load_traffic("bwd_dq", w.name,
+                                                  kernel_source_hash(["bwd_dq_bf16.hip", "ringx_device.h"]))},
+        "bwd_pre_bf16_kernel": {"ms": pre_ms, "bytes": B * H * Nq * (4 * d + 4),
+                                "GB/s": B * H * Nq * (4 * d + 4) / (pre_ms * 1e-3) / 1e9},
     }
-    dominant = "bwd" if bwd_ms >= fwd_ms else "fwd"
-    dom = kernels["bwd_pre+bwd_bf16"] if dominant == "bwd" else kernels["fwd_bf16"]
+    for name in ("fwd_bf16_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel"):
+        kernels[name]["frac"] = kernels[name]["tflops"] / PEAK_BF16_TFLOPS
+    dominant = max(("fwd_bf16_kernel", "bwd_dkdv_kernel", "bwd_dq_kernel"),
+                   key=lambda n: kernels[n]["ms"])
+    dom = kernels[dominant]
     roofline = {
-        "kernel": "bwd_bf16_kernel" if dominant == "bwd" else "fwd_bf16_kernel",
-        "bound": "mfma", "achieved": dom["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-        "frac": dom["frac"], "traffic": dom["traffic"],
-        "work_per_launch": f"{dom['flops']:.4e} flops ("
-                           + ("8*B*H*Nq*Nk*d: the backward's four contractions"
-                              if dominant == "bwd" else "4*B*H*Nq*Nk*d: the forward's two contractions")
-                           + ")",
+        "kernel": dominant, "bound": "mfma", "achieved": dom["tflops"], "peak": PEAK_BF16_TFLOPS,
+        "unit": "TFLOP/s", "frac": dom["frac"], "traffic": dom["traffic"],
+        "work_per_launch": f"{dom['flops']:.4e} flops = {dom['work']}",
     }
 
     # standalone Eq. (5) merge of the R per-chunk partials (an HBM-bound kernel)
@@ -246,7 +266,8 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name, "B": B, "H": H, "Nq": Nq, "Nk": Nk, "d": d, "R": R,
                    "flops_per_step": 6 * U, "flop_convention": "12*B*H*Nq*Nk*d per fwd+bwd step",
-                   "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
+                   "fwd_ms": fwd_ms, "bwd_ms": bwd_ms, "bwd_pre_ms": pre_ms,
+                   "bwd_dkdv_ms": dkdv_ms, "bwd_dq_ms": dq_ms,
                    "tflops_fa_convention_14": 7 * U / (ms_step * 1e-3) / 1e12},
         "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "roofline": roofline,

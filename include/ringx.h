@@ -95,25 +95,50 @@ ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void*
                              ringx_dtype out_dtype, hipStream_t stream);
 
 /*
- * Recompute-based backward with the merged lse (Sec. III-A, "Communication scheme": K/V chunk
- * gradients are computed per chunk, dQ accumulates over all N steps).  Softmax gradient:
+ * Recompute-based backward with the merged lse (Sec. III-A, "Communication scheme": the K/V
+ * chunk gradients are computed per chunk, the gradient of Q accumulates over all N steps).
+ * Softmax gradient:
  *   D_i = sum_c dout_ic out_ic;  P_ij = exp(scale q_i.k_j - lse_i);  dP_ij = dout_i . v_j;
  *   dS_ij = P_ij (dP_ij - D_i);  dV_j = sum_i P_ij dout_i;  dK_j = scale sum_i dS_ij q_i;
  *   dQ_i = scale sum_j dS_ij k_j.
+ * Runs ringx_bwd_preprocess, ringx_attn_bwd_dkdv and ringx_attn_bwd_dq in that order.
  *   q, k, v, out, dout (dtype), lse [B,H,Nq] fp32 (from ringx_attn_fwd or ringx_lse_merge).
- *   dq [B,H,Nq,d] fp32 -- overwritten; accumulated over every chunk in fp32.
+ *   dq [B,H,Nq,d] fp32 -- overwritten; accumulated over every chunk in fp32 registers.
  *   dk, dv [B,H,Nk,d] fp32 -- overwritten, or added to when accumulate_dkv != 0 (as dK/dV
  *   travelling around a ring collect the contributions of other query shards).
  *   workspace/workspace_bytes -- device scratch of at least ringx_bwd_workspace_bytes(...) bytes,
- *   16-byte aligned, owned by the caller; contents on entry are ignored.
+ *   16-byte aligned, owned by the caller; it receives D; contents on entry are ignored.
  *   R -- chunk count: no key tile straddles a chunk boundary; results do not depend on R beyond
- *   rounding.  dq is not bitwise reproducible (fp32 atomics); dk, dv are.
+ *   rounding.  dq, dk and dv are bitwise reproducible.
  */
 ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const void* out,
                             const void* dout, const float* lse, float* dq, float* dk, float* dv,
                             int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
                             float scale, ringx_dtype dtype, int accumulate_dkv, void* workspace,
                             size_t workspace_bytes, hipStream_t stream);
+
+/* Backward preprocess: delta[B,H,Nq] (fp32) = sum_c dout_ic out_ic for every query row.
+ *   out, dout [B,H,Nq,d] in dtype (d as for the forward).  delta is caller-owned. */
+ringx_status ringx_bwd_preprocess(const void* out, const void* dout, float* delta, int64_t B,
+                                  int64_t H, int64_t Nq, int64_t d, ringx_dtype dtype,
+                                  hipStream_t stream);
+
+/* Gradients of the keys and values (the part a RingX group reduces across ranks): for every key
+ * j of every chunk, dV_j = sum_i P_ij dout_i and dK_j = scale sum_i dS_ij q_i over all Nq queries,
+ * using lse and delta from ringx_bwd_preprocess.  dk, dv [B,H,Nk,d] fp32, overwritten or added
+ * to (accumulate_dkv != 0). */
+ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout,
+                                 const float* lse, const float* delta, float* dk, float* dv,
+                                 int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
+                                 int64_t R, float scale, ringx_dtype dtype, int accumulate_dkv,
+                                 hipStream_t stream);
+
+/* Gradient of the queries (the part each rank accumulates over all ring steps):
+ * dQ_i = scale sum_j dS_ij k_j over the keys of every chunk.  dq [B,H,Nq,d] fp32, overwritten. */
+ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, const void* dout,
+                               const float* lse, const float* delta, float* dq, int64_t B,
+                               int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                               float scale, ringx_dtype dtype, hipStream_t stream);
 
 /* Bytes of backward workspace for these arguments (0 if the arguments are invalid).  Host only. */
 size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,

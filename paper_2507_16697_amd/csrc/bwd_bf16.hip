@@ -1,19 +1,21 @@
-// Recompute backward of ring-chunked attention, bf16 MFMA with fp32 accumulation (gfx950).
+// Recompute backward of ring-chunked attention, dK/dV part: bf16 MFMA with fp32 accumulation
+// (gfx950).
 //
-// One workgroup = 4 waves = one (b, h) and a tile of 128 keys inside one chunk (a key tile never
-// straddles a chunk boundary).  Each wave owns 32 of those keys and keeps their K and V rows in
-// registers and their dK^T, dV^T accumulators in registers for the whole sweep over the query
-// tiles.  With the merged log-sum-exp saved by the forward, every chunk's gradients are
-// independent (arXiv 2507.16697 Sec. III-A: K/V chunk gradients per chunk, dQ accumulated over
-// all steps).  Per query tile of BQ queries:
-//   S   = Q K^T          A = Q rows (LDS),          B = K rows (registers)  -> lane = key
-//   dP  = dO V^T         A = dO rows (LDS),         B = V rows (registers)
-//   P   = exp(S*scale - lse_i),  dS = P (dP - D_i)               (fp32, exp2 domain)
-//   dV^T += dO^T P       A = dO^T (LDS, transposed), B = P from registers
-//   dK^T += Q^T dS       A = Q^T  (LDS, transposed), B = dS from registers
-//   dQ  += dS K          dS through LDS, A = dS rows, B = K^T (LDS); fp32 atomics into dq
-// The transposed Q/dO tiles use the same key/query order permutation as the forward's V^T tile,
-// so the 8 queries a lane feeds to the dV/dK MFMAs are one 16-byte LDS read.
+// One workgroup = 8 waves = one (b, h) and a tile of 128 keys inside one chunk (a key tile never
+// straddles a chunk boundary).  With the merged log-sum-exp saved by the forward, every chunk's
+// gradients are independent (arXiv 2507.16697 Sec. III-A: K/V chunk gradients computed per
+// chunk), so the workgroup sweeps every query tile of BQ queries once.  Wave w owns keys
+// 32*(w%4) .. +31 of the tile and query half w/4 of every query tile, and keeps fp32 dK^T, dV^T
+// accumulators for its keys in registers.  Per query tile:
+//   S   = Q K^T        A = Q rows (LDS),  B = K rows (LDS)              -> lane = key
+//   dP  = dO V^T       A = dO rows (LDS), B = V rows (LDS)
+//   P   = exp2(S*scale*log2e - lse_i*log2e),  dS = P (dP - D_i)        (fp32)
+//   dV^T += dO^T P     A = dO^T by transposed LDS reads, B = P from registers
+//   dK^T += Q^T dS     A = Q^T by transposed LDS reads,  B = dS from registers
+// Q, dO, lse and D of the next query tile arrive by direct global->LDS loads while the current
+// one is processed (double buffered, one barrier per tile).  K and V tiles are row-major in LDS
+// with XOR-swizzled 16-byte chunks.  The two waves sharing a key block add their dK/dV through
+// LDS at the end.  dQ is computed by the query-stationary kernel in bwd_dq_bf16.hip.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
@@ -21,119 +23,105 @@
 namespace ringx {
 namespace {
 
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
 template <int D>
-struct BwdCfg {
-  static constexpr int kThreads = 256;
-  static constexpr int kWaves = 4;
-  static constexpr int kBK = 128;                    // keys per workgroup (32 per wave)
-  static constexpr int kBQ = 4096 / D;               // queries per tile: 32 (d=128), 64 (d=64)
-  static constexpr int kQB = kBQ / 32;               // 32-query blocks per tile
+struct DkvCfg {
+  static constexpr int kThreads = 512;
+  static constexpr int kWaves = 8;
+  static constexpr int kBK = 128;                  // keys per workgroup (32 per key block)
+  static constexpr int kBQ = 8192 / D;             // queries per tile: 64 (d=128), 128 (d=64)
+  static constexpr int kQW = kBQ / 2;              // queries per wave
+  static constexpr int kQB = kQW / 32;             // 32-query blocks per wave
+  static constexpr int kRowBytes = 2 * D;          // Q, dO, K, V rows
   static constexpr int kDSteps = D / 16;
-  static constexpr int kQSteps = kBQ / 16;
   static constexpr int kCT = D / 32;
-  static constexpr int kRS = D + 8;                  // row stride of Q, dO tiles (elements)
-  static constexpr int kTS = kBQ + 8;                // row stride of Q^T, dO^T tiles
-  static constexpr int kKTS = kBK + 8;               // row stride of K^T and dS tiles
-  static constexpr int kDq4 = D / 4;                 // 4-dim groups per row
-  static_assert(kBQ * D == kThreads * 16, "each thread stages 4 queries x 4 dims");
-  static_assert(kQB * kCT == kWaves, "one 32x32 dQ tile per wave");
+  static constexpr int kQTile = kBQ * kRowBytes;   // bytes of one Q or dO tile (16 KiB)
+  static constexpr int kKTile = kBK * kRowBytes;   // bytes of the K or V tile
+  // LDS carve-up (bytes)
+  static constexpr int kOffK = 0;
+  static constexpr int kOffV = kOffK + kKTile;
+  static constexpr int kOffQ = kOffV + kKTile;          // 2 buffers
+  static constexpr int kOffO = kOffQ + 2 * kQTile;      // 2 buffers
+  static constexpr int kOffL = kOffO + 2 * kQTile;      // 2 x kBQ floats: lse
+  static constexpr int kOffD = kOffL + 2 * kBQ * 4;     // 2 x kBQ floats: D
+  static constexpr int kLds = kOffD + 2 * kBQ * 4;
+  static_assert(kQB * 32 * 2 == kBQ, "two query halves");
+  static_assert(4 * kQTile >= kWaves / 2 * kCT * 16 * 64 * 4, "dK/dV exchange fits");
 };
 
-__device__ __forceinline__ int perm16(int o) {
-  const int q4 = (o >> 2) & 3;
-  const int q4s = ((q4 & 1) << 1) | (q4 >> 1);
-  return (o & ~15) | (q4s << 2) | (o & 3);
+// XOR swizzle of the 16-byte chunks of a row of `RB` bytes (as in the forward kernel): 16
+// consecutive rows read at one chunk, and 4 consecutive rows read at 2 chunks by transposed
+// reads, hit distinct banks.
+template <int RB>
+__device__ __forceinline__ int swz(int row) {
+  if constexpr (RB == 256) return ((row & 3) << 2) | ((row >> 2) & 3);
+  else return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+}
+template <int RB>
+__device__ __forceinline__ int toff(int row, int c) {
+  return row * RB + ((c ^ swz<RB>(row)) << 4);
+}
+// byte offset of element `col` (2-byte units) of `row`
+template <int RB>
+__device__ __forceinline__ int eoff(int row, int col) {
+  return toff<RB>(row, col >> 3) + (col & 7) * 2;
 }
 
+// Rows row0 .. of a [N, D] bf16 matrix into a swizzled LDS tile at `dst` (rows clamped to
+// `last`), `per_wave` 1 KiB blocks per wave.
 template <int D>
-struct QStage {
-  u32x2 q[4];
-  u32x2 o[4];
-  float lse2;
-  float delta;
-};
-
-// Thread t stages query quad qq (4 rows) x dim quad dq4 (4 dims) of Q and dO.
-template <int D>
-__device__ __forceinline__ void load_q_tile(QStage<D>& st, const __bf16* __restrict__ qb,
-                                            const __bf16* __restrict__ ob,
-                                            const float* __restrict__ lseb,
-                                            const float* __restrict__ deltab, int64_t q0,
-                                            int64_t Nq, int t) {
-  using C = BwdCfg<D>;
-  const int dq4 = t % C::kDq4;
-  const int qq = t / C::kDq4;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int64_t qi = q0 + qq * 4 + e;
-    if (qi < Nq) {
-      st.q[e] = *reinterpret_cast<const u32x2*>(qb + qi * D + dq4 * 4);
-      st.o[e] = *reinterpret_cast<const u32x2*>(ob + qi * D + dq4 * 4);
-    } else {
-      st.q[e] = u32x2{0u, 0u};
-      st.o[e] = u32x2{0u, 0u};
-    }
-  }
-  if (t < C::kBQ) {
-    const int64_t qi = q0 + t;
-    st.lse2 = qi < Nq ? lseb[qi] * kLog2e : INFINITY;   // padded rows: P = exp2(-inf) = 0
-    st.delta = qi < Nq ? deltab[qi] : 0.f;
+__device__ __forceinline__ void issue_rows(const __bf16* __restrict__ src, uint32_t dst,
+                                           int64_t row0, int64_t last, int per_wave, int wave,
+                                           int lane, int nwaves) {
+  constexpr int kCh = D / 8;
+  for (int u = 0; u < per_wave; ++u) {
+    const int blk = u * nwaves + wave;
+    const int slot = blk * 64 + lane;
+    const int row = slot / kCh;
+    const int c = (slot % kCh) ^ swz<2 * D>(row);
+    int64_t r = row0 + row;
+    r = r < last ? r : last;
+    load_lds16(src + r * D + c * 8, dst + (uint32_t)__builtin_amdgcn_readfirstlane(blk * 1024));
   }
 }
 
-template <int D>
-__device__ __forceinline__ void store_q_tile(const QStage<D>& st, __bf16* qs, __bf16* os,
-                                             __bf16* qt, __bf16* ot, float* lse2s, float* ds,
-                                             int t) {
-  using C = BwdCfg<D>;
-  const int dq4 = t % C::kDq4;
-  const int qq = t / C::kDq4;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    *reinterpret_cast<u32x2*>(qs + (qq * 4 + e) * C::kRS + dq4 * 4) = st.q[e];
-    *reinterpret_cast<u32x2*>(os + (qq * 4 + e) * C::kRS + dq4 * 4) = st.o[e];
-  }
-  const int pos = perm16(qq * 4);
-#pragma unroll
-  for (int m = 0; m < 4; ++m) {
-    const int w = m >> 1;
-    const int sh = (m & 1) * 16;
-    u32x2 a, b;
-    a[0] = ((st.q[0][w] >> sh) & 0xffffu) | (((st.q[1][w] >> sh) & 0xffffu) << 16);
-    a[1] = ((st.q[2][w] >> sh) & 0xffffu) | (((st.q[3][w] >> sh) & 0xffffu) << 16);
-    b[0] = ((st.o[0][w] >> sh) & 0xffffu) | (((st.o[1][w] >> sh) & 0xffffu) << 16);
-    b[1] = ((st.o[2][w] >> sh) & 0xffffu) | (((st.o[3][w] >> sh) & 0xffffu) << 16);
-    *reinterpret_cast<u32x2*>(qt + (dq4 * 4 + m) * C::kTS + pos) = a;
-    *reinterpret_cast<u32x2*>(ot + (dq4 * 4 + m) * C::kTS + pos) = b;
-  }
-  if (t < C::kBQ) {
-    lse2s[t] = st.lse2;
-    ds[t] = st.delta;
+// lse and D of queries row0 .. row0 + BQ - 1 (clamped to `last`) into LDS, 4 bytes per lane:
+// waves 0 and 1 load lse, waves 2 and 3 load D.
+template <int BQ>
+__device__ __forceinline__ void issue_rowvals(const float* __restrict__ lseb,
+                                              const float* __restrict__ deltab, uint32_t ldst,
+                                              uint32_t ddst, int64_t row0, int64_t last,
+                                              int wave, int lane) {
+  static_assert(BQ <= 128, "two waves per array");
+  const int part = wave & 1;
+  if (wave < 4 && part * 64 < BQ) {
+    int64_t r = row0 + part * 64 + lane;
+    r = r < last ? r : last;
+    if (wave < 2)
+      load_lds4(lseb + r, ldst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
+    else
+      load_lds4(deltab + r, ddst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void bwd_bf16_kernel(
+__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse,
-    const float* __restrict__ delta, float* __restrict__ dq, float* __restrict__ dk,
-    float* __restrict__ dv, int BH, int64_t Nq, int64_t Nk, int R, int tiles_per_chunk,
-    float c2, float scale, int accumulate) {
-  using C = BwdCfg<D>;
-  __shared__ __attribute__((aligned(16))) __bf16 kt_s[D * C::kKTS];       // K^T of the key tile
-  __shared__ __attribute__((aligned(16))) __bf16 q_s[C::kBQ * C::kRS];
-  __shared__ __attribute__((aligned(16))) __bf16 o_s[C::kBQ * C::kRS];
-  __shared__ __attribute__((aligned(16))) __bf16 qt_s[D * C::kTS];
-  __shared__ __attribute__((aligned(16))) __bf16 ot_s[D * C::kTS];
-  __shared__ __attribute__((aligned(16))) __bf16 ds_s[C::kBQ * C::kKTS];  // dS [query][key]
-  __shared__ __attribute__((aligned(16))) float lse2_s[C::kBQ];
-  __shared__ __attribute__((aligned(16))) float d_s[C::kBQ];
+    const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BH,
+    int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale, int accumulate) {
+  using C = DkvCfg<D>;
+  __shared__ __attribute__((aligned(1024))) char lds[C::kLds];
+  const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = t >> 6;
   const int n = lane & 31;
   const int g = lane >> 5;
+  const int kb = wave & 3;          // key block of this wave
+  const int qh = wave >> 2;         // query half of this wave
 
   const uint32_t wg = xcd_remap(blockIdx.x, gridDim.x);
   const int64_t per_bh = (int64_t)R * tiles_per_chunk;
@@ -149,45 +137,45 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(
 
   const __bf16* qb = q + bh * Nq * D;
   const __bf16* ob = dout + bh * Nq * D;
-  const __bf16* kb = k + bh * Nk * D;
-  const __bf16* vb = v + bh * Nk * D;
+  const __bf16* kbp = k + bh * Nk * D;
+  const __bf16* vbp = v + bh * Nk * D;
   const float* lseb = lse + bh * Nq;
   const float* deltab = delta + bh * Nq;
-  float* dqb = dq + bh * Nq * D;
 
-  // this lane's key: column of S, dP and of the dK^T/dV^T accumulators
-  const int jl = wave * 32 + n;
-  const bool key_ok = jl < nvalid;
-  bf16x8 kf[C::kDSteps], vf[C::kDSteps];
-  {
-    const int64_t key = k0 + (key_ok ? jl : 0);
+  const int64_t nqt = (Nq + C::kBQ - 1) / C::kBQ;
+
+  // K and V tiles (kept for the whole sweep), then the first query tile
+  issue_rows<D>(kbp, lbase + C::kOffK, k0, hi - 1, C::kKTile / 1024 / C::kWaves, wave, lane,
+                C::kWaves);
+  issue_rows<D>(vbp, lbase + C::kOffV, k0, hi - 1, C::kKTile / 1024 / C::kWaves, wave, lane,
+                C::kWaves);
+  issue_rows<D>(qb, lbase + C::kOffQ, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
+                C::kWaves);
+  issue_rows<D>(ob, lbase + C::kOffO, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
+                C::kWaves);
+  issue_rowvals<C::kBQ>(lseb, deltab, lbase + C::kOffL, lbase + C::kOffD, 0, Nq - 1, wave, lane);
+  const float* lds_l = reinterpret_cast<const float*>(lds + C::kOffL);
+  const float* lds_d = reinterpret_cast<const float*>(lds + C::kOffD);
+
+  // per-lane LDS byte offsets (tile-relative)
+  // S / dP: A = Q/dO rows (query qh*kQW + 32*b + n), B = K/V rows (key 32*kb + n); chunk 2s+g
+  int aoff[C::kDSteps];
 #pragma unroll
-    for (int s = 0; s < C::kDSteps; ++s) {
-      kf[s] = *reinterpret_cast<const bf16x8*>(kb + key * D + s * 16 + g * 8);
-      vf[s] = *reinterpret_cast<const bf16x8*>(vb + key * D + s * 16 + g * 8);
-    }
-  }
-  // K^T tile (dims x keys, natural key order), zero for keys past the chunk end
-  for (int item = t; item < (C::kBK / 4) * C::kDq4; item += C::kThreads) {
-    const int dq4 = item % C::kDq4;
-    const int kq = item / C::kDq4;
-    u32x2 x[4];
+  for (int s = 0; s < C::kDSteps; ++s) aoff[s] = toff<2 * D>(n, 2 * s + g);   // + row block
+  // transposed reads of Q/dO (rows = queries, cols = dims): 16-lane group G reads rows
+  // j0 + (lane%16)/4 with j0 = 4g + 8h (+16*ks), columns 32*ct + 16*(G&1) + 4*(lane%4); lane i
+  // of the group receives rows j0..j0+3 of column 32*ct + 16*(G&1) + i.
+  const int G = lane >> 4;
+  const int trr = (lane & 15) >> 2;
+  const int trc = 16 * (G & 1) + 4 * (lane & 3);
+  int qtoff[2][C::kCT];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int jj = kq * 4 + e;
-      x[e] = jj < nvalid ? *reinterpret_cast<const u32x2*>(kb + (k0 + jj) * D + dq4 * 4)
-                         : u32x2{0u, 0u};
-    }
+  for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const int w = m >> 1;
-      const int sh = (m & 1) * 16;
-      u32x2 a;
-      a[0] = ((x[0][w] >> sh) & 0xffffu) | (((x[1][w] >> sh) & 0xffffu) << 16);
-      a[1] = ((x[2][w] >> sh) & 0xffffu) | (((x[3][w] >> sh) & 0xffffu) << 16);
-      *reinterpret_cast<u32x2*>(kt_s + (dq4 * 4 + m) * C::kKTS + kq * 4) = a;
-    }
-  }
+    for (int ct = 0; ct < C::kCT; ++ct)
+      qtoff[h][ct] = eoff<2 * D>(4 * g + 8 * h + trr, 32 * ct + trc);
+
+  const bool key_ok = 32 * kb + n < nvalid;
 
   f32x16 dvt[C::kCT], dkt[C::kCT];
 #pragma unroll
@@ -196,22 +184,31 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(
     dkt[c] = f32x16{};
   }
 
-  const int64_t nqt = (Nq + C::kBQ - 1) / C::kBQ;
-  QStage<D> st;
-  load_q_tile<D>(st, qb, ob, lseb, deltab, 0, Nq, t);
-
-  // this wave's dQ output tile
-  const int dq_qb = wave / C::kCT;
-  const int dq_ct = wave % C::kCT;
+  wait_vmem_all();
+  __syncthreads();
 
   for (int64_t it = 0; it < nqt; ++it) {
+    const int cur = (int)(it & 1);
     const int64_t q0 = it * C::kBQ;
-    __syncthreads();   // previous tile's LDS reads are done
-    store_q_tile<D>(st, q_s, o_s, qt_s, ot_s, lse2_s, d_s, t);
-    __syncthreads();
-    if (it + 1 < nqt) load_q_tile<D>(st, qb, ob, lseb, deltab, q0 + C::kBQ, Nq, t);
+    // next query tile in flight: Q, dO rows and their lse, D straight into LDS
+    if (it + 1 < nqt) {
+      const int64_t q1 = q0 + C::kBQ;
+      issue_rows<D>(qb, lbase + C::kOffQ + (cur ^ 1) * C::kQTile, q1, Nq - 1,
+                    C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
+      issue_rows<D>(ob, lbase + C::kOffO + (cur ^ 1) * C::kQTile, q1, Nq - 1,
+                    C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
+      issue_rowvals<C::kBQ>(lseb, deltab, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
+                            lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, q1, Nq - 1, wave, lane);
+    }
+    const bool ragged = q0 + C::kBQ > Nq;   // last tile: rows past Nq are clamped copies
+    const char* qt = lds + C::kOffQ + cur * C::kQTile;
+    const char* ot = lds + C::kOffO + cur * C::kQTile;
+    const char* kt = lds + C::kOffK;
+    const char* vt = lds + C::kOffV;
+    const float* cl = lds_l + cur * C::kBQ;
+    const float* cd = lds_d + cur * C::kBQ;
 
-    // S = Q K^T and dP = dO V^T  (lane = key n, rows = queries)
+    // S = Q K^T, dP = dO V^T for this wave's 32 keys and kQW queries
     f32x16 sacc[C::kQB], pacc[C::kQB];
 #pragma unroll
     for (int b = 0; b < C::kQB; ++b) {
@@ -220,116 +217,123 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(
     }
 #pragma unroll
     for (int s = 0; s < C::kDSteps; ++s) {
+      const bf16x8 bk = *reinterpret_cast<const bf16x8*>(kt + (32 * kb) * C::kRowBytes + aoff[s]);
+      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(vt + (32 * kb) * C::kRowBytes + aoff[s]);
 #pragma unroll
       for (int b = 0; b < C::kQB; ++b) {
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(q_s + (b * 32 + n) * C::kRS + s * 16 + g * 8);
-        const bf16x8 ao = *reinterpret_cast<const bf16x8*>(o_s + (b * 32 + n) * C::kRS + s * 16 + g * 8);
-        sacc[b] = mfma32(aq, kf[s], sacc[b]);
-        pacc[b] = mfma32(ao, vf[s], pacc[b]);
+        const int rowb = (qh * C::kQW + 32 * b) * C::kRowBytes;
+        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(qt + rowb + aoff[s]);
+        const bf16x8 ao = *reinterpret_cast<const bf16x8*>(ot + rowb + aoff[s]);
+        sacc[b] = mfma32(aq, bk, sacc[b]);
+        pacc[b] = mfma32(ao, bv, pacc[b]);
       }
     }
-    // P and dS (fp32), packed to bf16 B operands; dS also goes to LDS for dQ
-    bf16x8 pf[C::kQSteps], sf[C::kQSteps];
+    // P and dS (fp32) -> bf16 B operands.  Accumulator r of block b is query
+    // 32b + 8(r/4) + 4g + r%4; the 8 queries of k-step 2b+h are accumulators 8h .. 8h+7.
+    bf16x8 pf[2 * C::kQB], sf[2 * C::kQB];
 #pragma unroll
     for (int b = 0; b < C::kQB; ++b) {
+      float p[16], dsv[16];
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int qi = qh * C::kQW + 32 * b + 8 * rq + 4 * g;   // 4 consecutive queries
+        const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + qi) * -kLog2e;
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(cd + qi);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float pe = fast_exp2(__builtin_fmaf(sacc[b][4 * rq + e], c2, nl4[e]));
+          pe = key_ok ? pe : 0.f;
+          if (ragged && q0 + qi + e >= Nq) pe = 0.f;
+          p[4 * rq + e] = pe;
+          dsv[4 * rq + e] = pe * (pacc[b][4 * rq + e] - d4[e]);
+        }
+      }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         u32x4 wp, ws;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          float p2[2], s2[2];
-#pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int rr = 8 * h + 2 * e + u;
-            const int qi = b * 32 + 8 * (rr >> 2) + 4 * g + (rr & 3);
-            float p = fast_exp2(__builtin_fmaf(sacc[b][rr], c2, -lse2_s[qi]));
-            p = key_ok ? p : 0.f;
-            p2[u] = p;
-            s2[u] = p * (pacc[b][rr] - d_s[qi]);
-          }
-          wp[e] = pack_bf16x2(p2[0], p2[1]);
-          ws[e] = pack_bf16x2(s2[0], s2[1]);
+          wp[e] = pack_bf16x2(p[8 * h + 2 * e], p[8 * h + 2 * e + 1]);
+          ws[e] = pack_bf16x2(dsv[8 * h + 2 * e], dsv[8 * h + 2 * e + 1]);
         }
         pf[2 * b + h] = __builtin_bit_cast(bf16x8, wp);
         sf[2 * b + h] = __builtin_bit_cast(bf16x8, ws);
-        // dS to LDS, [query][key]
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int rr0 = 8 * h + 2 * e;
-          const int qa = b * 32 + 8 * (rr0 >> 2) + 4 * g + (rr0 & 3);
-          const uint32_t w = ws[e];
-          *reinterpret_cast<uint16_t*>(ds_s + qa * C::kKTS + jl) = (uint16_t)(w & 0xffffu);
-          *reinterpret_cast<uint16_t*>(ds_s + (qa + 1) * C::kKTS + jl) = (uint16_t)(w >> 16);
-        }
       }
     }
     // dV^T += dO^T P, dK^T += Q^T dS
 #pragma unroll
-    for (int s = 0; s < C::kQSteps; ++s) {
+    for (int ks = 0; ks < 2 * C::kQB; ++ks) {
+      const int rowb = (qh * C::kQW + 16 * ks) * C::kRowBytes;
 #pragma unroll
       for (int c = 0; c < C::kCT; ++c) {
-        const bf16x8 ao = *reinterpret_cast<const bf16x8*>(ot_s + (c * 32 + n) * C::kTS + s * 16 + g * 8);
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(qt_s + (c * 32 + n) * C::kTS + s * 16 + g * 8);
-        dvt[c] = mfma32(ao, pf[s], dvt[c]);
-        dkt[c] = mfma32(aq, sf[s], dkt[c]);
+        const bf16x4 o0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + qtoff[0][c]));
+        const bf16x4 o1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + qtoff[1][c]));
+        const bf16x4 q0v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + qtoff[0][c]));
+        const bf16x4 q1v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + qtoff[1][c]));
+        dvt[c] = mfma32(__builtin_shufflevector(o0, o1, 0, 1, 2, 3, 4, 5, 6, 7), pf[ks], dvt[c]);
+        dkt[c] = mfma32(__builtin_shufflevector(q0v, q1v, 0, 1, 2, 3, 4, 5, 6, 7), sf[ks], dkt[c]);
       }
     }
-    __syncthreads();   // dS tile complete
-    // dQ tile (queries dq_qb*32.., dims dq_ct*32..) = dS K over the workgroup's 128 keys
-    f32x16 qacc = f32x16{};
-#pragma unroll
-    for (int s = 0; s < C::kBK / 16; ++s) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(ds_s + (dq_qb * 32 + n) * C::kKTS + s * 16 + g * 8);
-      const bf16x8 b = *reinterpret_cast<const bf16x8*>(kt_s + (dq_ct * 32 + n) * C::kKTS + s * 16 + g * 8);
-      qacc = mfma32(a, b, qacc);
-    }
-#pragma unroll
-    for (int rr = 0; rr < 16; ++rr) {
-      const int64_t qi = q0 + dq_qb * 32 + 8 * (rr >> 2) + 4 * g + (rr & 3);
-      if (qi < Nq) unsafeAtomicAdd(dqb + qi * D + dq_ct * 32 + n, qacc[rr] * scale);
-    }
+    // next tile landed (the only vector memory operations in flight); this tile's reads done
+    wait_vmem_all();
+    __syncthreads();
   }
 
-  // dK = scale * dK^T^T, dV = dV^T^T for this lane's key
-  if (key_ok) {
-    const int64_t key = k0 + jl;
-    float* dkr = dk + (bh * Nk + key) * D;
-    float* dvr = dv + (bh * Nk + key) * D;
+  // the two query halves of a key block add their dK^T / dV^T through LDS
+  float* xch = reinterpret_cast<float*>(lds + C::kOffQ);
+  const int64_t key = k0 + 32 * kb + n;
+  float* dkr = dk + (bh * Nk + key) * D;
+  float* dvr = dv + (bh * Nk + key) * D;
 #pragma unroll
-    for (int c = 0; c < C::kCT; ++c)
+  for (int which = 0; which < 2; ++which) {
+    f32x16* acc = which == 0 ? dkt : dvt;
+    if (qh == 1) {
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int col = c * 32 + 8 * rq + 4 * g;
-        f32x4 kv = {dkt[c][4 * rq] * scale, dkt[c][4 * rq + 1] * scale,
-                    dkt[c][4 * rq + 2] * scale, dkt[c][4 * rq + 3] * scale};
-        f32x4 vv = {dvt[c][4 * rq], dvt[c][4 * rq + 1], dvt[c][4 * rq + 2], dvt[c][4 * rq + 3]};
-        if (accumulate) {
-          kv += *reinterpret_cast<const f32x4*>(dkr + col);
-          vv += *reinterpret_cast<const f32x4*>(dvr + col);
-        }
-        *reinterpret_cast<f32x4*>(dkr + col) = kv;
-        *reinterpret_cast<f32x4*>(dvr + col) = vv;
+      for (int c = 0; c < C::kCT; ++c)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) xch[((kb * C::kCT + c) * 16 + rr) * 64 + lane] = acc[c][rr];
+    }
+    __syncthreads();
+    if (qh == 0) {
+#pragma unroll
+      for (int c = 0; c < C::kCT; ++c)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) acc[c][rr] += xch[((kb * C::kCT + c) * 16 + rr) * 64 + lane];
+      if (key_ok) {
+        float* dst = which == 0 ? dkr : dvr;
+        const float f = which == 0 ? scale : 1.0f;
+#pragma unroll
+        for (int c = 0; c < C::kCT; ++c)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq) {
+            const int col = c * 32 + 8 * rq + 4 * g;
+            f32x4 val = {acc[c][4 * rq] * f, acc[c][4 * rq + 1] * f, acc[c][4 * rq + 2] * f,
+                         acc[c][4 * rq + 3] * f};
+            if (accumulate) val += *reinterpret_cast<const f32x4*>(dst + col);
+            *reinterpret_cast<f32x4*>(dst + col) = val;
+          }
       }
+    }
+    __syncthreads();
   }
 }
 
 template <int D>
 hipError_t launch(const BwdArgs& a) {
-  using C = BwdCfg<D>;
+  using C = DkvCfg<D>;
   const int64_t max_chunk = (a.Nk + a.R - 1) / a.R;
   const int64_t tpc = (max_chunk + C::kBK - 1) / C::kBK;
   const int64_t nwg = a.BH * a.R * tpc;
-  hipLaunchKernelGGL((bwd_bf16_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (const __bf16*)a.dout, a.lse, a.delta, a.dq, a.dk, a.dv, (int)a.BH, a.Nq,
-                     a.Nk, (int)a.R, (int)tpc, a.scale * kLog2e, a.scale,
-                     a.accumulate_dkv ? 1 : 0);
+                     (const __bf16*)a.dout, a.lse, a.delta, a.dk, a.dv, (int)a.BH, a.Nq, a.Nk,
+                     (int)a.R, (int)tpc, a.scale * kLog2e, a.scale, a.accumulate_dkv ? 1 : 0);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_bwd_bf16(const BwdArgs& a) {
+hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a) {
   if (a.d == 128) return launch<128>(a);
   return launch<64>(a);
 }

@@ -95,14 +95,17 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_dq_kernel(
 }
 
 template <int DMAX>
-hipError_t launch(const BwdArgs& a) {
+hipError_t launch_dkdv(const BwdArgs& a) {
   const dim3 gk((uint32_t)((a.Nk + kThreads - 1) / kThreads), (uint32_t)a.BH);
   hipLaunchKernelGGL((bwd_f32_dkdv_kernel<DMAX>), gk, dim3(kThreads), 0, a.stream,
                      (const float*)a.q, (const float*)a.k, (const float*)a.v,
                      (const float*)a.dout, a.lse, a.delta, a.dk, a.dv, a.Nq, a.Nk, (int)a.d,
                      a.scale, a.accumulate_dkv ? 1 : 0);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+template <int DMAX>
+hipError_t launch_dq(const BwdArgs& a) {
   const dim3 gq((uint32_t)((a.Nq + kThreads - 1) / kThreads), (uint32_t)a.BH);
   hipLaunchKernelGGL((bwd_f32_dq_kernel<DMAX>), gq, dim3(kThreads), 0, a.stream,
                      (const float*)a.q, (const float*)a.k, (const float*)a.v,
@@ -112,10 +115,16 @@ hipError_t launch(const BwdArgs& a) {
 
 }  // namespace
 
-hipError_t launch_bwd_f32(const BwdArgs& a) {
-  if (a.d <= 32) return launch<32>(a);
-  if (a.d <= 64) return launch<64>(a);
-  return launch<128>(a);
+hipError_t launch_bwd_dkdv_f32(const BwdArgs& a) {
+  if (a.d <= 32) return launch_dkdv<32>(a);
+  if (a.d <= 64) return launch_dkdv<64>(a);
+  return launch_dkdv<128>(a);
+}
+
+hipError_t launch_bwd_dq_f32(const BwdArgs& a) {
+  if (a.d <= 32) return launch_dq<32>(a);
+  if (a.d <= 64) return launch_dq<64>(a);
+  return launch_dq<128>(a);
 }
 
 }  // namespace ringx

@@ -1,9 +1,7 @@
-// Backward preprocess: D_i = sum_c dout_ic * out_ic (fp32) for every query row, and dq := 0.
+// Backward preprocess: D_i = sum_c dout_ic * out_ic (fp32) for every query row.
 //
-// The recompute backward needs D_i for dS_ij = P_ij (dP_ij - D_i).  dq is cleared here because
-// the main backward kernel accumulates into it with fp32 atomics (a plain store kernel, so the
-// sequence stays free of memset nodes if a caller captures it in a graph).  HBM-bound: reads
-// out and dout once, writes D and dq once.
+// The recompute backward needs D_i for dS_ij = P_ij (dP_ij - D_i).  HBM-bound: reads out and
+// dout once, writes D once.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
@@ -17,7 +15,7 @@ constexpr int kPreThreads = 256;
 template <int D>
 __global__ __launch_bounds__(kPreThreads) void bwd_pre_bf16_kernel(
     const __bf16* __restrict__ out, const __bf16* __restrict__ dout, float* __restrict__ delta,
-    float* __restrict__ dq, int64_t rows) {
+    int64_t rows) {
   constexpr int kTpr = D / 8;
   const int64_t idx = (int64_t)blockIdx.x * kPreThreads + threadIdx.x;
   const int64_t row = idx / kTpr;
@@ -31,9 +29,6 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_bf16_kernel(
       s = __builtin_fmaf(bf16_lo(o[w]), bf16_lo(g[w]), s);
       s = __builtin_fmaf(bf16_hi(o[w]), bf16_hi(g[w]), s);
     }
-    f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    *reinterpret_cast<f32x4*>(dq + row * D + part * 8) = z;
-    *reinterpret_cast<f32x4*>(dq + row * D + part * 8 + 4) = z;
   }
 #pragma unroll
   for (int off = kTpr / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, kTpr);
@@ -42,14 +37,11 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_bf16_kernel(
 
 __global__ __launch_bounds__(kPreThreads) void bwd_pre_f32_kernel(
     const float* __restrict__ out, const float* __restrict__ dout, float* __restrict__ delta,
-    float* __restrict__ dq, int64_t rows, int d) {
+    int64_t rows, int d) {
   const int64_t row = (int64_t)blockIdx.x * kPreThreads + threadIdx.x;
   if (row >= rows) return;
   float s = 0.f;
-  for (int c = 0; c < d; ++c) {
-    s = __builtin_fmaf(out[row * d + c], dout[row * d + c], s);
-    dq[row * d + c] = 0.f;
-  }
+  for (int c = 0; c < d; ++c) s = __builtin_fmaf(out[row * d + c], dout[row * d + c], s);
   delta[row] = s;
 }
 
@@ -62,14 +54,14 @@ hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16) {
     const dim3 grid((uint32_t)((n + kPreThreads - 1) / kPreThreads));
     if (a.d == 128)
       hipLaunchKernelGGL(bwd_pre_bf16_kernel<128>, grid, dim3(kPreThreads), 0, a.stream,
-                         (const __bf16*)a.out, (const __bf16*)a.dout, a.delta, a.dq, rows);
+                         (const __bf16*)a.out, (const __bf16*)a.dout, a.delta, rows);
     else
       hipLaunchKernelGGL(bwd_pre_bf16_kernel<64>, grid, dim3(kPreThreads), 0, a.stream,
-                         (const __bf16*)a.out, (const __bf16*)a.dout, a.delta, a.dq, rows);
+                         (const __bf16*)a.out, (const __bf16*)a.dout, a.delta, rows);
   } else {
     const dim3 grid((uint32_t)((rows + kPreThreads - 1) / kPreThreads));
     hipLaunchKernelGGL(bwd_pre_f32_kernel, grid, dim3(kPreThreads), 0, a.stream,
-                       (const float*)a.out, (const float*)a.dout, a.delta, a.dq, rows, (int)a.d);
+                       (const float*)a.out, (const float*)a.dout, a.delta, rows, (int)a.d);
   }
   return hipGetLastError();
 }

@@ -58,15 +58,6 @@ __device__ __forceinline__ int tile_off(int row, int c) {   // byte offset
   return row * (D * 2) + ((c ^ swz<D>(row)) << 4);
 }
 
-// One 16-byte direct global->LDS load per lane: LDS destination = lds_base + 16 * lane.
-// Issued through inline asm so that the compiler does not order later LDS reads of the other
-// buffer behind it; the explicit vmcnt wait before the workgroup barrier publishes the tile.
-__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(lds_base), "v"(gptr)
-               : "memory", "m0");
-}
 
 // Issue the direct loads of one K/V tile: rows start..start+kBK-1 (clamped to hi-1).
 template <int D>
@@ -90,7 +81,6 @@ __device__ __forceinline__ void issue_tile(const __bf16* __restrict__ kb,
   }
 }
 
-__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 template <int D, bool PARTIALS>
 __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
@@ -180,7 +170,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
   float lse2m = -INFINITY;  // merged log2-sum-exp over finished chunks
 
   int cur = 0;
-  wait_vm_all();
+  wait_vmem_all();
   __syncthreads();
 
   while (true) {
@@ -343,7 +333,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
     }
 
     if (!has_next) break;
-    wait_vm_all();
+    wait_vmem_all();
     __syncthreads();
     cur ^= 1;
     start = nstart;

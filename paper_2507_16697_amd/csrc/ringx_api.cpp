@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <initializer_list>
 
 #include "ringx.h"
 #include "ringx_kernels.h"
@@ -160,6 +161,85 @@ ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void*
   return hip_status(ringx::launch_lse_merge(a));
 }
 
+
+ringx_status ringx_bwd_preprocess(const void* out, const void* dout, float* delta, int64_t B,
+                                  int64_t H, int64_t Nq, int64_t d, ringx_dtype dtype,
+                                  hipStream_t stream) {
+  if (!out || !dout || !delta) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, 1, d, 1, 1.0f, dtype);
+  if (st != RINGX_OK) return st;
+  for (const void* p : {out, dout, (const void*)delta})
+    if (!aligned16(p)) return RINGX_E_ALIGN;
+  const int64_t es = esize(dtype), bh = B * H;
+  const Span sd = span(delta, bh * Nq * 4);
+  if (overlap(sd, span(out, bh * Nq * d * es)) || overlap(sd, span(dout, bh * Nq * d * es)))
+    return RINGX_E_ALIAS;
+  ringx::BwdArgs a{nullptr, nullptr, nullptr, out, dout, nullptr, nullptr, nullptr, nullptr,
+                   delta, bh, Nq, 1, d, 1, 1.0f, false, stream};
+  return hip_status(ringx::launch_bwd_pre(a, dtype == RINGX_BF16));
+}
+
+namespace {
+
+// Shared validation of the two gradient stages; `outs` are the fp32 outputs being written.
+ringx_status check_bwd_stage(const void* q, const void* k, const void* v, const void* dout,
+                             const float* lse, const float* delta,
+                             std::initializer_list<Span> outs, int64_t B, int64_t H, int64_t Nq,
+                             int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype) {
+  if (!q || !k || !v || !dout || !lse || !delta) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  for (const void* p : {q, k, v, dout, (const void*)lse, (const void*)delta})
+    if (!aligned16(p)) return RINGX_E_ALIGN;
+  for (const Span& o : outs)
+    if ((o.lo & 15u) != 0) return RINGX_E_ALIGN;
+  const int64_t es = esize(dtype), bh = B * H;
+  const Span ins[] = {span(q, bh * Nq * d * es), span(k, bh * Nk * d * es),
+                      span(v, bh * Nk * d * es), span(dout, bh * Nq * d * es),
+                      span(lse, bh * Nq * 4), span(delta, bh * Nq * 4)};
+  for (auto oi = outs.begin(); oi != outs.end(); ++oi) {
+    for (const Span& i : ins)
+      if (overlap(*oi, i)) return RINGX_E_ALIAS;
+    for (auto oj = oi + 1; oj != outs.end(); ++oj)
+      if (overlap(*oi, *oj)) return RINGX_E_ALIAS;
+  }
+  return RINGX_OK;
+}
+
+}  // namespace
+
+ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout,
+                                 const float* lse, const float* delta, float* dk, float* dv,
+                                 int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
+                                 int64_t R, float scale, ringx_dtype dtype, int accumulate_dkv,
+                                 hipStream_t stream) {
+  if (!dk || !dv) return RINGX_E_NULLPTR;
+  const int64_t bh = B * H;
+  ringx_status st = check_bwd_stage(q, k, v, dout, lse, delta,
+                                    {span(dk, bh * Nk * d * 4), span(dv, bh * Nk * d * 4)}, B, H,
+                                    Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  ringx::BwdArgs a{q,  k,  v,  nullptr, dout, lse,   nullptr, dk, dv, const_cast<float*>(delta),
+                   bh, Nq, Nk, d,       R,    scale, accumulate_dkv != 0, stream};
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dkdv_bf16(a)
+                                        : ringx::launch_bwd_dkdv_f32(a));
+}
+
+ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, const void* dout,
+                               const float* lse, const float* delta, float* dq, int64_t B,
+                               int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                               float scale, ringx_dtype dtype, hipStream_t stream) {
+  if (!dq) return RINGX_E_NULLPTR;
+  const int64_t bh = B * H;
+  ringx_status st = check_bwd_stage(q, k, v, dout, lse, delta, {span(dq, bh * Nq * d * 4)}, B, H,
+                                    Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  ringx::BwdArgs a{q,  k,  v,  nullptr, dout, lse,   dq,    nullptr, nullptr,
+                   const_cast<float*>(delta), bh, Nq, Nk, d, R, scale, false, stream};
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dq_bf16(a)
+                                        : ringx::launch_bwd_dq_f32(a));
+}
+
 size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
                                  int64_t R, ringx_dtype dtype) {
   if (check_dims(B, H, Nq, Nk, d, R, 1.0f, dtype) != RINGX_OK) return 0;
@@ -192,12 +272,14 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
     for (int j = i + 1; j < 4; ++j)
       if (overlap(outs[i], outs[j])) return RINGX_E_ALIAS;
   }
-  ringx::BwdArgs a{q,  k,  v,  out, dout, lse,   dq, dk, dv, static_cast<float*>(workspace),
+  float* delta = static_cast<float*>(workspace);
+  ringx::BwdArgs a{q,  k,  v,  out, dout, lse,   dq, dk, dv, delta,
                    bh, Nq, Nk, d,   R,    scale, accumulate_dkv != 0, stream};
   const bool bf16 = dtype == RINGX_BF16;
-  hipError_t e = ringx::launch_bwd_pre(a, bf16);
-  if (e != hipSuccess) return RINGX_E_HIP;
-  return hip_status(bf16 ? ringx::launch_bwd_bf16(a) : ringx::launch_bwd_f32(a));
+  if (ringx::launch_bwd_pre(a, bf16) != hipSuccess) return RINGX_E_HIP;
+  if ((bf16 ? ringx::launch_bwd_dkdv_bf16(a) : ringx::launch_bwd_dkdv_f32(a)) != hipSuccess)
+    return RINGX_E_HIP;
+  return hip_status(bf16 ? ringx::launch_bwd_dq_bf16(a) : ringx::launch_bwd_dq_f32(a));
 }
 
 }  // extern "C"

@@ -56,4 +56,29 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t w, uint32_t n) {
   return (w % kXcd) * per + w / kXcd;
 }
 
+// One 16-byte direct global->LDS load per lane (global_load_lds_dwordx4): the LDS destination is
+// lds_base + 16 * lane.  Issued through inline asm so that the compiler does not serialise later
+// LDS reads of other buffers behind it.  The asm sets m0, which the compiler never uses in these
+// kernels (a build test checks the generated code); callers publish the data with
+// wait_vmem_all() followed by a workgroup barrier.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(gptr)
+               : "memory", "m0");
+}
+// Same with 4 bytes per lane: LDS destination = lds_base + 4 * lane.
+__device__ __forceinline__ void load_lds4(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+               :
+               : "s"(lds_base), "v"(gptr)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(0): every vector memory load of this wave (including direct LDS loads) done.
+__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 }  // namespace ringx

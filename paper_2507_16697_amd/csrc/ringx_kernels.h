@@ -40,7 +40,7 @@ struct BwdArgs {
   float* dq;
   float* dk;
   float* dv;
-  float* delta;       // workspace: D_i = dout_i . out_i, [B,H,Nq]
+  float* delta;       // D_i = dout_i . out_i, [B,H,Nq]
   int64_t BH, Nq, Nk, d, R;
   float scale;
   bool accumulate_dkv;
@@ -51,8 +51,10 @@ hipError_t launch_fwd_bf16(const FwdArgs& a, bool partials);
 hipError_t launch_fwd_f32(const FwdArgs& a, bool partials);
 hipError_t launch_lse_merge(const MergeArgs& a);
 hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16);
-hipError_t launch_bwd_bf16(const BwdArgs& a);
-hipError_t launch_bwd_f32(const BwdArgs& a);
+hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a);
+hipError_t launch_bwd_dq_bf16(const BwdArgs& a);
+hipError_t launch_bwd_dkdv_f32(const BwdArgs& a);
+hipError_t launch_bwd_dq_f32(const BwdArgs& a);
 
 int64_t fwd_bf16_workgroups(int64_t BH, int64_t Nq, int64_t d);
 

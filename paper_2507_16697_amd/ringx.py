@@ -30,6 +30,7 @@ STATUS_NAMES = {
 }
 
 EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "ringx_attn_bwd",
+            "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv", "ringx_attn_bwd_dq",
             "ringx_bwd_workspace_bytes", "ringx_chunk_bounds", "ringx_status_str")
 
 
@@ -60,13 +61,19 @@ def lib() -> ctypes.CDLL:
         L.ringx_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                      ctypes.c_float, ctypes.c_int, ctypes.c_int, _P,
                                      ctypes.c_size_t, _P]
+        L.ringx_bwd_preprocess.argtypes = [_P, _P, _P, _I, _I, _I, _I, ctypes.c_int, _P]
+        L.ringx_attn_bwd_dkdv.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
+                                          ctypes.c_float, ctypes.c_int, ctypes.c_int, _P]
+        L.ringx_attn_bwd_dq.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
+                                        ctypes.c_float, ctypes.c_int, _P]
         L.ringx_bwd_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, ctypes.c_int]
         L.ringx_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.ringx_chunk_bounds.argtypes = [_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
         L.ringx_status_str.argtypes = [ctypes.c_int]
         L.ringx_status_str.restype = ctypes.c_char_p
         for name in ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge",
-                     "ringx_attn_bwd", "ringx_chunk_bounds"):
+                     "ringx_attn_bwd", "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv",
+                     "ringx_attn_bwd_dq", "ringx_chunk_bounds"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -209,3 +216,54 @@ def ringx_attn_bwd(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None
                               workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ringx_attn_bwd", st)
     return dq, dk, dv
+
+
+def ringx_bwd_preprocess(out, dout, delta=None, stream=None):
+    """delta [B,H,Nq] fp32 = rowsum(dout * out)."""
+    torch = _torch()
+    _dev(out, dout)
+    B, H, Nq, d = out.shape
+    if delta is None:
+        delta = torch.empty((B, H, Nq), dtype=torch.float32, device=out.device)
+    _dev(delta)
+    st = lib().ringx_bwd_preprocess(out.data_ptr(), dout.data_ptr(), delta.data_ptr(), B, H, Nq,
+                                    d, _dtype_code(out), _stream(stream))
+    _check("ringx_bwd_preprocess", st)
+    return delta
+
+
+def ringx_attn_bwd_dkdv(q, k, v, dout, lse, delta, R: int, scale=None, dk=None, dv=None,
+                        accumulate_dkv=False, stream=None):
+    """Key/value gradients of every chunk.  Returns fp32 (dk, dv)."""
+    torch = _torch()
+    _dev(q, k, v, dout, lse, delta)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    f32 = dict(dtype=torch.float32, device=q.device)
+    if dk is None:
+        dk = torch.zeros((B, H, Nk, d), **f32)
+    if dv is None:
+        dv = torch.zeros((B, H, Nk, d), **f32)
+    _dev(dk, dv)
+    st = lib().ringx_attn_bwd_dkdv(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
+                                   lse.data_ptr(), delta.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+                                   B, H, Nq, Nk, d, R, _scale(scale, d), _dtype_code(q),
+                                   1 if accumulate_dkv else 0, _stream(stream))
+    _check("ringx_attn_bwd_dkdv", st)
+    return dk, dv
+
+
+def ringx_attn_bwd_dq(q, k, v, dout, lse, delta, R: int, scale=None, dq=None, stream=None):
+    """Query gradient accumulated over every chunk.  Returns fp32 dq."""
+    torch = _torch()
+    _dev(q, k, v, dout, lse, delta)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    if dq is None:
+        dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
+    _dev(dq)
+    st = lib().ringx_attn_bwd_dq(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
+                                 lse.data_ptr(), delta.data_ptr(), dq.data_ptr(), B, H, Nq, Nk, d,
+                                 R, _scale(scale, d), _dtype_code(q), _stream(stream))
+    _check("ringx_attn_bwd_dq", st)
+    return dq

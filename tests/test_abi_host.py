@@ -131,3 +131,33 @@ def test_backward_validation():
     assert bwd(dq=QP) == ALIAS                      # dq over q
     assert bwd(dk=OP) == ALIAS                      # dk over dq
     assert bwd(ws=OP + 16 * GB) == ALIAS            # workspace over dv
+
+
+def pre(o=QP, do=KP, dl=LP, B=1, H=2, Nq=100, d=64, dt=BF16):
+    return ringx.lib().ringx_bwd_preprocess(o, do, dl, B, H, Nq, d, dt, None)
+
+
+def test_preprocess_validation():
+    assert pre(o=0) == NULLPTR and pre(dl=0) == NULLPTR
+    assert pre(B=0) == SHAPE and pre(d=96) == UNSUP
+    assert pre(dl=LP + 4) == ALIGN
+    assert pre(dl=QP) == ALIAS
+
+
+def dkdv(dk=OP, dv=OP + 8 * GB, lse=LP, delta=LP + 8 * GB, R=3, d=64, acc=0):
+    return ringx.lib().ringx_attn_bwd_dkdv(QP, KP, VP, QP + 16 * GB, lse, delta, dk, dv, 1, 2, 100,
+                                           300, d, R, 0.125, BF16, acc, None)
+
+
+def dqs(dq=OP, lse=LP, delta=LP + 8 * GB, R=3, d=64):
+    return ringx.lib().ringx_attn_bwd_dq(QP, KP, VP, QP + 16 * GB, lse, delta, dq, 1, 2, 100, 300,
+                                         d, R, 0.125, BF16, None)
+
+
+def test_gradient_stage_validation():
+    assert dkdv(dk=0) == NULLPTR and dkdv(delta=0) == NULLPTR and dqs(dq=0) == NULLPTR
+    assert dkdv(R=301) == CHUNKS and dqs(R=0) == CHUNKS
+    assert dkdv(d=80) == UNSUP and dqs(d=80) == UNSUP
+    assert dkdv(dv=OP + 8 * GB + 4) == ALIGN and dqs(dq=OP + 8) == ALIGN
+    assert dkdv(dv=OP) == ALIAS and dkdv(dk=KP) == ALIAS and dqs(dq=LP) == ALIAS
+    assert dqs(dq=LP + 8 * GB) == ALIAS    # dq over delta

@@ -294,16 +294,35 @@ def test_bf16_backward_accumulate_and_invariants():
     torch.cuda.synchronize()
     assert torch.allclose(dk2 - base_k, dk, rtol=0, atol=1e-5)
     assert torch.allclose(dv2 - base_v, dv, rtol=0, atol=1e-5)
-    # dk and dv are written by plain stores: bitwise reproducible
-    _, dk3, dv3 = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    # no atomics anywhere: every gradient is bitwise reproducible
+    dq3, dk3, dv3 = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
     torch.cuda.synchronize()
-    assert torch.equal(dk3, dk) and torch.equal(dv3, dv)
+    assert torch.equal(dq3, dq) and torch.equal(dk3, dk) and torch.equal(dv3, dv)
     # sum_j dV_j = sum_i dO_i and sum_j dK_j = 0, per (b, h)
     sdv = dv.double().sum(dim=2)
     sdo = g["do"].double().sum(dim=2)
     assert torch.max(torch.abs(sdv - sdo)) <= 2e-2 * torch.max(torch.abs(dv.double()).sum(dim=2))
     sdk = dk.double().sum(dim=2)
     assert torch.max(torch.abs(sdk)) <= 2e-2 * torch.max(torch.abs(dk.double()).sum(dim=2))
+
+
+@pytest.mark.parametrize("dtype,d", [(torch.bfloat16, 128), (torch.bfloat16, 64), (torch.float32, 24)])
+def test_backward_stages_compose(dtype, d):
+    """ringx_attn_bwd is exactly ringx_bwd_preprocess + ringx_attn_bwd_dkdv + ringx_attn_bwd_dq."""
+    B, H, Nq, Nk, R = 1, 2, 130, 333, 3
+    store = "bf16" if dtype == torch.bfloat16 else "fp32"
+    t, x = random_case(24, B, H, Nq, Nk, d, store=store, std=0.6)
+    g = _dev(t, store)
+    scale = float(np.float32(1 / math.sqrt(d)))
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    delta = ringx.ringx_bwd_preprocess(out, g["do"])
+    dk2, dv2 = ringx.ringx_attn_bwd_dkdv(g["q"], g["k"], g["v"], g["do"], lse, delta, R, scale=scale)
+    dq2 = ringx.ringx_attn_bwd_dq(g["q"], g["k"], g["v"], g["do"], lse, delta, R, scale=scale)
+    torch.cuda.synchronize()
+    assert torch.equal(dq, dq2) and torch.equal(dk, dk2) and torch.equal(dv, dv2)
+    ref_d = (to_host_f64(out) * x["do"]).sum(axis=-1)
+    assert max_abs_err(to_host_f64(delta), ref_d) <= 1e-4 * max(1.0, float(np.abs(ref_d).max()))
 
 
 def test_errors_leave_outputs_untouched():
