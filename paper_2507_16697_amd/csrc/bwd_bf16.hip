@@ -200,7 +200,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
       issue_rowvals<C::kBQ>(lseb, deltab, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
                             lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, q1, Nq - 1, wave, lane);
     }
-    const bool ragged = q0 + C::kBQ > Nq;   // last tile: rows past Nq are clamped copies
+    // last query tile (rows past Nq are clamped copies) or a partial key tile
+    const bool masked = q0 + C::kBQ > Nq || nvalid < C::kBK;
     const char* qt = lds + C::kOffQ + cur * C::kQTile;
     const char* ot = lds + C::kOffO + cur * C::kQTile;
     const char* kt = lds + C::kOffK;
@@ -241,11 +242,21 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
         const f32x4 d4 = *reinterpret_cast<const f32x4*>(cd + qi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          float pe = fast_exp2(__builtin_fmaf(sacc[b][4 * rq + e], c2, nl4[e]));
-          pe = key_ok ? pe : 0.f;
-          if (ragged && q0 + qi + e >= Nq) pe = 0.f;
+          const float pe = fast_exp2(__builtin_fmaf(sacc[b][4 * rq + e], c2, nl4[e]));
           p[4 * rq + e] = pe;
           dsv[4 * rq + e] = pe * (pacc[b][4 * rq + e] - d4[e]);
+        }
+      }
+      if (masked) {
+        // keys past the chunk end (one lane each) and queries past Nq (clamped copies) add nothing
+        cold_path();
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int qi = qh * C::kQW + 32 * b + 8 * (rr >> 2) + 4 * g + (rr & 3);
+          if (!key_ok || q0 + qi >= Nq) {
+            p[rr] = 0.f;
+            dsv[rr] = 0.f;
+          }
         }
       }
 #pragma unroll

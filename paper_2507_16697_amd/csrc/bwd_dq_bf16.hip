@@ -50,22 +50,49 @@ __device__ __forceinline__ int tile_off(int row, int c) {
 }
 
 template <int D>
-__device__ __forceinline__ void issue_tile(const __bf16* __restrict__ kb,
-                                           const __bf16* __restrict__ vb, uint32_t kdst,
-                                           uint32_t vdst, int64_t start, int64_t hi, int wave,
-                                           int lane) {
+__device__ __forceinline__ void load_offsets(int (&goff)[DqCfg<D>::kLoads],
+                                             int (&grow)[DqCfg<D>::kLoads], int wave, int lane) {
   using C = DqCfg<D>;
 #pragma unroll
   for (int u = 0; u < C::kLoads; ++u) {
     const int slot = (u * C::kWaves + wave) * 64 + lane;
     const int row = slot / C::kChunks;
     const int c = (slot % C::kChunks) ^ swz<D>(row);
-    int64_t key = start + row;
-    key = key < hi ? key : hi - 1;
-    const uint32_t wbase =
-        (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
-    load_lds16(kb + key * D + c * 8, kdst + wbase);
-    load_lds16(vb + key * D + c * 8, vdst + wbase);
+    grow[u] = row;
+    goff[u] = row * C::kRowBytes + c * 16;
+  }
+}
+
+// Direct loads of one K/V tile starting at key `start`; rows at or past `hi` (only in the last
+// tile of a chunk) are clamped to hi - 1.
+template <int D>
+__device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
+                                           const char* __restrict__ vb, uint32_t kdst,
+                                           uint32_t vdst, int64_t start, int64_t hi,
+                                           const int (&goff)[DqCfg<D>::kLoads],
+                                           const int (&grow)[DqCfg<D>::kLoads], int wave) {
+  using C = DqCfg<D>;
+  const char* kt = kb + start * C::kRowBytes;
+  const char* vt = vb + start * C::kRowBytes;
+  if (start + C::kBK <= hi) {
+#pragma unroll
+    for (int u = 0; u < C::kLoads; ++u) {
+      const uint32_t wbase =
+          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
+      load_lds16(kt + goff[u], kdst + wbase);
+      load_lds16(vt + goff[u], vdst + wbase);
+    }
+  } else {
+    cold_path();
+    const int last = (int)(hi - 1 - start);
+#pragma unroll
+    for (int u = 0; u < C::kLoads; ++u) {
+      const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
+      const uint32_t wbase =
+          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
+      load_lds16(kt + off, kdst + wbase);
+      load_lds16(vt + off, vdst + wbase);
+    }
   }
 }
 
@@ -91,8 +118,10 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
   const int64_t q0 = (wg % nqt) * C::kBQ + wave * C::kQW;
   if (bh >= BH) return;
 
-  const __bf16* kb = k + bh * Nk * D;
-  const __bf16* vb = v + bh * Nk * D;
+  const char* kb = reinterpret_cast<const char*>(k + bh * Nk * D);
+  const char* vb = reinterpret_cast<const char*>(v + bh * Nk * D);
+  int goff[C::kLoads], grow[C::kLoads];
+  load_offsets<D>(goff, grow, wave, lane);
 
   // chunk bookkeeping without divisions (see the forward kernel)
   const int64_t q_sz = Nk / R;
@@ -105,7 +134,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
 
   const uint32_t lk = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_k;
   const uint32_t lv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_v;
-  issue_tile<D>(kb, vb, lk, lv, start, hi, wave, lane);
+  issue_tile<D>(kb, vb, lk, lv, start, hi, goff, grow, wave);
 
   // this lane's query: Q and dO fragments (B operands), -lse*log2e and D
   int64_t qi = q0 + n;
@@ -165,7 +194,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
     }
     if (has_next)
       issue_tile<D>(kb, vb, lk + (cur ^ 1) * C::kTileBytes, lv + (cur ^ 1) * C::kTileBytes,
-                    nstart, nhi, wave, lane);
+                    nstart, nhi, goff, grow, wave);
 
     const char* kbuf = lds_k + cur * C::kTileBytes;
     const char* vbuf = lds_v + cur * C::kTileBytes;
@@ -189,6 +218,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
       }
     }
     if (nvalid < C::kBK) {
+      cold_path();
 #pragma unroll
       for (int kt = 0; kt < C::kKTiles; ++kt)
 #pragma unroll

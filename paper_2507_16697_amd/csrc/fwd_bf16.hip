@@ -59,28 +59,54 @@ __device__ __forceinline__ int tile_off(int row, int c) {   // byte offset
 }
 
 
-// Issue the direct loads of one K/V tile: rows start..start+kBK-1 (clamped to hi-1).
+// Per-lane byte offsets (from the tile's first row) of this lane's direct loads: 16-byte slot
+// `slot` of the swizzled tile holds logical chunk (slot % chunks) ^ swz(row) of row slot / chunks.
 template <int D>
-__device__ __forceinline__ void issue_tile(const __bf16* __restrict__ kb,
-                                           const __bf16* __restrict__ vb, uint32_t kdst,
-                                           uint32_t vdst, int64_t start, int64_t hi, int wave,
-                                           int lane) {
+__device__ __forceinline__ void load_offsets(int (&goff)[FwdCfg<D>::kLoads],
+                                             int (&grow)[FwdCfg<D>::kLoads], int wave, int lane) {
   using C = FwdCfg<D>;
 #pragma unroll
   for (int u = 0; u < C::kLoads; ++u) {
-    const int slot = (u * C::kWaves + wave) * 64 + lane;      // 16-byte LDS slot
+    const int slot = (u * C::kWaves + wave) * 64 + lane;
     const int row = slot / C::kChunks;
-    const int pc = slot % C::kChunks;
-    const int c = pc ^ swz<D>(row);
-    int64_t key = start + row;
-    key = key < hi ? key : hi - 1;
-    const uint32_t wbase =
-        (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
-    load_lds16(kb + key * D + c * 8, kdst + wbase);
-    load_lds16(vb + key * D + c * 8, vdst + wbase);
+    const int c = (slot % C::kChunks) ^ swz<D>(row);
+    grow[u] = row;
+    goff[u] = row * C::kRowBytes + c * 16;
   }
 }
 
+// Issue the direct loads of one K/V tile starting at key `start`; rows at or past `hi` (only in
+// the last tile of a chunk) are clamped to hi - 1.
+template <int D>
+__device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
+                                           const char* __restrict__ vb, uint32_t kdst,
+                                           uint32_t vdst, int64_t start, int64_t hi,
+                                           const int (&goff)[FwdCfg<D>::kLoads],
+                                           const int (&grow)[FwdCfg<D>::kLoads], int wave) {
+  using C = FwdCfg<D>;
+  const char* kt = kb + start * C::kRowBytes;
+  const char* vt = vb + start * C::kRowBytes;
+  if (start + C::kBK <= hi) {
+#pragma unroll
+    for (int u = 0; u < C::kLoads; ++u) {
+      const uint32_t wbase =
+          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
+      load_lds16(kt + goff[u], kdst + wbase);
+      load_lds16(vt + goff[u], vdst + wbase);
+    }
+  } else {
+    cold_path();
+    const int last = (int)(hi - 1 - start);
+#pragma unroll
+    for (int u = 0; u < C::kLoads; ++u) {
+      const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
+      const uint32_t wbase =
+          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
+      load_lds16(kt + off, kdst + wbase);
+      load_lds16(vt + off, vdst + wbase);
+    }
+  }
+}
 
 template <int D, bool PARTIALS>
 __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
@@ -104,8 +130,10 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
   if (bh >= BH) return;
 
   const __bf16* qb = q + bh * Nq * D;
-  const __bf16* kb = k + bh * Nk * D;
-  const __bf16* vb = v + bh * Nk * D;
+  const char* kb = reinterpret_cast<const char*>(k + bh * Nk * D);
+  const char* vb = reinterpret_cast<const char*>(v + bh * Nk * D);
+  int goff[C::kLoads], grow[C::kLoads];
+  load_offsets<D>(goff, grow, wave, lane);
 
   // chunk bookkeeping without divisions: chunk r has q_sz + (1 if the running remainder wraps)
   const int64_t q_sz = Nk / R;
@@ -126,7 +154,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
   const uint32_t lv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_v;
 
   // first tile in flight while Q is loaded
-  issue_tile<D>(kb, vb, lk, lv, start, hi, wave, lane);
+  issue_tile<D>(kb, vb, lk, lv, start, hi, goff, grow, wave);
 
   // Q fragments (B operand of S^T = K Q^T): query n of this wave, dims 16*ks + 8g .. +8.
   bf16x8 qf[C::kDSteps];
@@ -191,7 +219,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
     }
     if (has_next)
       issue_tile<D>(kb, vb, lk + (cur ^ 1) * C::kTileBytes, lv + (cur ^ 1) * C::kTileBytes,
-                    nstart, nhi, wave, lane);
+                    nstart, nhi, goff, grow, wave);
 
     const char* kbuf = lds_k + cur * C::kTileBytes;
     const char* vbuf = lds_v + cur * C::kTileBytes;
@@ -219,6 +247,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2 * C::kKTiles, 0);
     if (nvalid < C::kBK) {
+      cold_path();
 #pragma unroll
       for (int kt = 0; kt < C::kKTiles; ++kt)
 #pragma unroll
@@ -241,6 +270,7 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
     const float mt = mx * c2;
     const bool need = mt > m2 + kLazy;
     if (__builtin_amdgcn_ballot_w64(need)) {
+      cold_path();
       const float mnew = need ? mt : m2;
       const float alpha = fast_exp2(m2 - mnew);
       m2 = mnew;

@@ -78,6 +78,10 @@ __device__ __forceinline__ void load_lds4(const void* gptr, uint32_t lds_base) {
 }
 #pragma clang diagnostic pop
 
+// Keeps a rarely taken branch a branch: an empty volatile asm statement has side effects, so the
+// compiler cannot speculate the branch body into straight-line selects executed on every tile.
+__device__ __forceinline__ void cold_path() { asm volatile(""); }
+
 // s_waitcnt vmcnt(0): every vector memory load of this wave (including direct LDS loads) done.
 __device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
