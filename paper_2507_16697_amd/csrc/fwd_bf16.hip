@@ -1,14 +1,14 @@
 // Ring-chunked attention forward, bf16 storage, bf16 MFMA with fp32 accumulation (gfx950).
 //
 // One workgroup = 4 waves = one (b, h) and a tile of 128 queries (32 per wave).  The key/value
-// sequence is visited as R chunks (ring steps, arXiv 2507.16697 Sec. III-A); every chunk is
-// streamed through LDS in tiles of BK keys, double buffered (the on-chip analogue of the paper's
-// ping-pong buffers) and filled by direct global->LDS loads issued one tile ahead.  Within a chunk
-// each wave keeps an online softmax (Eqs. (2)-(4)); at the end of the chunk it forms the chunk's
-// local result (loc_out, loc_lse) and folds it into the running Eq. (5) merge held in registers.
-// PARTIALS = true writes the local results instead of merging them.
+// sequence is visited as R chunks (ring steps, arXiv 2507.16697 Sec. III-A), streamed through LDS
+// in tiles of 64 keys that never straddle a chunk boundary.  K and V tiles are double buffered
+// (the on-chip analogue of the paper's ping-pong buffers) and filled by direct global->LDS loads:
+// while tile j is processed, the K tile j+2 and the V tile j+1 are in flight.
 //
-// Per wave, with g = lane / 32 and n = lane % 32:
+// Each wave is software pipelined over key tiles: the MFMAs of S_{j+1} = K_{j+1} Q^T are
+// interleaved with the exponentials and row sums of tile j, and the MFMAs of O += V_j^T P_j with
+// the row maximum of S_{j+1}, so that the matrix cores and the vector ALU work at the same time.  Per wave, with g = lane / 32 and n = lane % 32:
 //   S^T = K Q^T   A = K rows from LDS (key n, 8 dims), B = Q^T from registers (query n, 8 dims)
 //                 -> lane holds query n and keys 8*(r/4) + 4g + r%4 of each 32-key block;
 //   O^T += V^T P^T A = V^T read from the row-major V tile with ds_read_b64_tr_b16 (4 keys per
@@ -16,12 +16,21 @@
 // LDS tiles are row-major with the 16-byte chunks of each row XOR-swizzled by the row index, so
 // that both the 16-byte K reads (16 rows, one chunk) and the transposed V reads (4 rows x 2
 // chunks per 16 lanes) hit distinct banks.
+//
 // Softmax statistics are fp32 in the exp2 domain (t = scale*log2(e)*q.k).  The reference maximum
 // of a row only moves when a tile's maximum exceeds it by more than kLazy (probabilities stay
-// below 2^kLazy), so the accumulator rescale is skipped for most tiles.
+// below 2^kLazy), so the accumulator rescale is skipped for most tiles.  At the end of chunk r the
+// wave forms the chunk's log-sum-exp loc_lse_r from the chunk's own row sum and folds it into the
+// merged lse by Eq. (5).  The output numerator is kept unnormalised: Eq. (5)'s term
+// exp(loc_lse_r - M) loc_out_r equals exp(m - M) times the chunk's unnormalised accumulator, so
+// one accumulator holds the running sum of all chunk terms and the final division by the Eq. (5)
+// denominator is a multiplication by 2^(m - lse).  PARTIALS = true instead writes every chunk's
+// (loc_out_r, loc_lse_r) and restarts the accumulator.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
+
+#include <type_traits>
 
 namespace ringx {
 namespace {
@@ -36,10 +45,10 @@ struct FwdCfg {
   static constexpr int kWaves = 4;
   static constexpr int kQW = 32;                  // queries per wave
   static constexpr int kBQ = kWaves * kQW;        // queries per workgroup
-  static constexpr int kBK = 8192 / D;            // keys per tile: 64 (d=128) or 128 (d=64)
+  static constexpr int kBK = 64;                  // keys per tile
   static constexpr int kRowBytes = D * 2;
   static constexpr int kChunks = D / 8;           // 16-byte chunks per row
-  static constexpr int kTileBytes = kBK * kRowBytes;   // 16 KiB
+  static constexpr int kTileBytes = kBK * kRowBytes;   // 16 KiB (d=128), 8 KiB (d=64)
   static constexpr int kKTiles = kBK / 32;        // 32-key blocks per tile
   static constexpr int kDSteps = D / 16;          // MFMA k-steps over the head dim
   static constexpr int kKSteps = kBK / 16;        // MFMA k-steps over the keys
@@ -75,38 +84,57 @@ __device__ __forceinline__ void load_offsets(int (&goff)[FwdCfg<D>::kLoads],
   }
 }
 
-// Issue the direct loads of one K/V tile starting at key `start`; rows at or past `hi` (only in
-// the last tile of a chunk) are clamped to hi - 1.
+// Issue the direct loads of one K or V tile starting at key `start` into the LDS buffer at
+// `dst`; rows at or past `hi` (only in the last tile of a chunk) are clamped to hi - 1.
 template <int D>
-__device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
-                                           const char* __restrict__ vb, uint32_t kdst,
-                                           uint32_t vdst, int64_t start, int64_t hi,
+__device__ __forceinline__ void issue_tile(const char* __restrict__ base, uint32_t dst,
+                                           int64_t start, int64_t hi,
                                            const int (&goff)[FwdCfg<D>::kLoads],
                                            const int (&grow)[FwdCfg<D>::kLoads], int wave) {
   using C = FwdCfg<D>;
-  const char* kt = kb + start * C::kRowBytes;
-  const char* vt = vb + start * C::kRowBytes;
+  const char* src = base + start * C::kRowBytes;
   if (start + C::kBK <= hi) {
 #pragma unroll
-    for (int u = 0; u < C::kLoads; ++u) {
-      const uint32_t wbase =
-          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
-      load_lds16(kt + goff[u], kdst + wbase);
-      load_lds16(vt + goff[u], vdst + wbase);
-    }
+    for (int u = 0; u < C::kLoads; ++u)
+      load_lds16(src + goff[u],
+                 dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024));
   } else {
     cold_path();
     const int last = (int)(hi - 1 - start);
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
       const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
-      const uint32_t wbase =
-          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
-      load_lds16(kt + off, kdst + wbase);
-      load_lds16(vt + off, vdst + wbase);
+      load_lds16(src + off,
+                 dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024));
     }
   }
 }
+
+// The chunked key sequence, walked one tile at a time (chunk r = [floor(r Nk/R), floor((r+1) Nk/R))
+// without divisions: chunk r has Nk/R keys plus one when the running remainder wraps).
+struct KeyTile {
+  int64_t start, hi;   // first key of the tile, end of its chunk; start >= Nk: no tile
+};
+
+struct ChunkWalk {
+  int64_t Nk, q_sz, rem, racc;
+  int R;
+  __device__ KeyTile first() {
+    racc = rem;
+    const int64_t extra = racc >= R ? 1 : 0;
+    racc -= extra * R;
+    return {0, q_sz + extra};
+  }
+  template <int BK>
+  __device__ KeyTile next(const KeyTile& t) {
+    if (t.start + BK < t.hi) return {t.start + BK, t.hi};
+    if (t.hi >= Nk) return {Nk, Nk};
+    racc += rem;
+    const int64_t extra = racc >= R ? 1 : 0;
+    racc -= extra * R;
+    return {t.hi, t.hi + q_sz + extra};
+  }
+};
 
 template <int D, bool PARTIALS>
 __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
@@ -135,26 +163,20 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
   int goff[C::kLoads], grow[C::kLoads];
   load_offsets<D>(goff, grow, wave, lane);
 
-  // chunk bookkeeping without divisions: chunk r has q_sz + (1 if the running remainder wraps)
-  const int64_t q_sz = Nk / R;
-  const int64_t rem = Nk % R;
-  int64_t racc = 0;   // (r * rem) mod R
-  int r = 0;
-  int64_t start = 0;
-  int64_t hi;
-  {
-    racc += rem;
-    const int64_t extra = racc >= R ? 1 : 0;
-    racc -= extra * R;
-    hi = q_sz + extra;
-  }
+  ChunkWalk walk{Nk, Nk / R, Nk % R, 0, R};
+  KeyTile t0 = walk.first();
+  KeyTile t1 = walk.next<C::kBK>(t0);
+  KeyTile t2 = walk.next<C::kBK>(t1);
+  int r0 = 0;   // chunk of t0
 
   // LDS byte addresses of the two K and two V buffers
   const uint32_t lk = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_k;
   const uint32_t lv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_v;
 
-  // first tile in flight while Q is loaded
-  issue_tile<D>(kb, vb, lk, lv, start, hi, goff, grow, wave);
+  // K_0, V_0 and K_1 in flight while Q is loaded
+  issue_tile<D>(kb, lk, t0.start, t0.hi, goff, grow, wave);
+  issue_tile<D>(vb, lv, t0.start, t0.hi, goff, grow, wave);
+  if (t1.start < Nk) issue_tile<D>(kb, lk + C::kTileBytes, t1.start, t1.hi, goff, grow, wave);
 
   // Q fragments (B operand of S^T = K Q^T): query n of this wave, dims 16*ks + 8g .. +8.
   bf16x8 qf[C::kDSteps];
@@ -187,152 +209,151 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
   }
 
   f32x16 oacc[C::kCT];
-  f32x16 om[C::kCT];
 #pragma unroll
-  for (int c = 0; c < C::kCT; ++c) {
-    oacc[c] = f32x16{};
-    om[c] = f32x16{};
-  }
-  float m2 = -INFINITY;     // reference max of the row within the chunk (exp2 domain)
-  float l = 0.f;            // this lane's share of the running sum within the chunk
-  float lse2m = -INFINITY;  // merged log2-sum-exp over finished chunks
+  for (int c = 0; c < C::kCT; ++c) oacc[c] = f32x16{};
+  float m2 = -INFINITY;     // reference max of the row (exp2 domain)
+  float lc = 0.f;           // this lane's share of the chunk's row sum, relative to m2
+  float lse2m = -INFINITY;  // merged log2-sum-exp over finished chunks (Eq. (5))
 
-  int cur = 0;
   wait_vmem_all();
   __syncthreads();
 
-  while (true) {
-    // next tile: the following BK keys of this chunk, or the first tile of the next chunk
-    int64_t nstart = start + C::kBK;
-    int64_t nhi = hi;
-    bool has_next = true;
-    if (nstart >= hi) {
-      if (r + 1 < R) {
-        nstart = hi;
-        racc += rem;
-        const int64_t extra = racc >= R ? 1 : 0;
-        racc -= extra * R;
-        nhi = hi + q_sz + extra;
-      } else {
-        has_next = false;
-      }
-    }
-    if (has_next)
-      issue_tile<D>(kb, vb, lk + (cur ^ 1) * C::kTileBytes, lv + (cur ^ 1) * C::kTileBytes,
-                    nstart, nhi, goff, grow, wave);
+  // S_0
+  f32x16 sa[C::kKTiles], sb[C::kKTiles];
+#pragma unroll
+  for (int kt = 0; kt < C::kKTiles; ++kt) sa[kt] = f32x16{};
+#pragma unroll
+  for (int s = 0; s < C::kDSteps; ++s)
+#pragma unroll
+    for (int kt = 0; kt < C::kKTiles; ++kt)
+      sa[kt] = mfma32(*reinterpret_cast<const bf16x8*>(lds_k + koff[s] + kt * 32 * C::kRowBytes),
+                      qf[s], sa[kt]);
+  float mx = -INFINITY;   // row max of the tile in `cur` (raw scores)
+#pragma unroll
+  for (int kt = 0; kt < C::kKTiles; ++kt)
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, sa[kt][rr]);
+  mx = max_halves(mx);
 
-    const char* kbuf = lds_k + cur * C::kTileBytes;
-    const char* vbuf = lds_v + cur * C::kTileBytes;
-    const int nvalid = (int)min<int64_t>(C::kBK, hi - start);
+  // One pipelined iteration for tile t0 (scores in `cur`); parity P selects the buffers: K_{j+1}
+  // is read from K buffer 1-P, V_j from V buffer P; K_{j+2} lands in K buffer P, V_{j+1} in V
+  // buffer 1-P.  Returns true after the last tile.
+  auto step = [&](f32x16 (&cur)[C::kKTiles], f32x16 (&nxt)[C::kKTiles], auto parity) -> bool {
+    constexpr int P = decltype(parity)::value;
+    // K_{j+1} and V_j landed (issued one iteration ago); every wave is done with K_j, V_{j-1}
+    wait_vmem_all();
+    __syncthreads();
+    if (t2.start < Nk)
+      issue_tile<D>(kb, lk + P * C::kTileBytes, t2.start, t2.hi, goff, grow, wave);
+    if (t1.start < Nk)
+      issue_tile<D>(vb, lv + (1 - P) * C::kTileBytes, t1.start, t1.hi, goff, grow, wave);
 
-    // S^T = K Q^T for the tile's 32-key blocks
-    f32x16 sacc[C::kKTiles];
-#pragma unroll
-    for (int kt = 0; kt < C::kKTiles; ++kt) sacc[kt] = f32x16{};
-#pragma unroll
-    for (int s = 0; s < C::kDSteps; ++s) {
-#pragma unroll
-      for (int kt = 0; kt < C::kKTiles; ++kt) {
-        const bf16x8 a =
-            *reinterpret_cast<const bf16x8*>(kbuf + koff[s] + kt * 32 * C::kRowBytes);
-        sacc[kt] = mfma32(a, qf[s], sacc[kt]);
-      }
-    }
-    // keep two k-steps of K fragments in flight ahead of the MFMAs
-    __builtin_amdgcn_sched_group_barrier(0x100, 2 * C::kKTiles, 0);
-#pragma unroll
-    for (int s = 0; s < C::kDSteps - 2; ++s) {
-      __builtin_amdgcn_sched_group_barrier(0x100, C::kKTiles, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, C::kKTiles, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2 * C::kKTiles, 0);
+    // last tile of a chunk: keys past the chunk end (clamped copies of its last key) add nothing.
+    // The row max needs no mask: a copy's score equals that of a valid key.
+    const int nvalid = (int)min<int64_t>(C::kBK, t0.hi - t0.start);
     if (nvalid < C::kBK) {
       cold_path();
+      const int thr = nvalid - 4 * g;   // key 4g + off is past the end iff off >= thr
 #pragma unroll
       for (int kt = 0; kt < C::kKTiles; ++kt)
 #pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int key = kt * 32 + 8 * (rr >> 2) + 4 * g + (rr & 3);
-          if (key >= nvalid) sacc[kt][rr] = -INFINITY;
-        }
+        for (int rr = 0; rr < 16; ++rr)
+          if (kt * 32 + 8 * (rr >> 2) + (rr & 3) >= thr) cur[kt][rr] = -INFINITY;
     }
-    // online softmax within the chunk (Eqs. (2)-(3) with a lazily moved reference max)
-    float mx = -INFINITY;
+    // lazily moved reference max (Eqs. (2)-(3))
+    {
+      const float mt = mx * c2;
+      const bool need = mt > m2 + kLazy;
+      if (__builtin_amdgcn_ballot_w64(need)) {
+        cold_path();
+        const float mnew = need ? mt : m2;
+        const float alpha = fast_exp2(m2 - mnew);
+        m2 = mnew;
+        lc *= alpha;
+#pragma unroll
+        for (int c = 0; c < C::kCT; ++c) oacc[c] *= alpha;
+      }
+    }
+
+    // S_{j+1} = K_{j+1} Q^T on the matrix cores, P_j = exp2(t - m) on the vector ALU
+    const char* kbuf = lds_k + (1 - P) * C::kTileBytes;
+#pragma unroll
+    for (int kt = 0; kt < C::kKTiles; ++kt) nxt[kt] = f32x16{};
+#pragma unroll
+    for (int s = 0; s < C::kDSteps; ++s)
+#pragma unroll
+      for (int kt = 0; kt < C::kKTiles; ++kt)
+        nxt[kt] = mfma32(*reinterpret_cast<const bf16x8*>(kbuf + koff[s] + kt * 32 * C::kRowBytes),
+                         qf[s], nxt[kt]);
+    bf16x8 pf[C::kKSteps];
+    float la = 0.f, lb = 0.f;
 #pragma unroll
     for (int kt = 0; kt < C::kKTiles; ++kt)
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, sacc[kt][rr]);
-    {
-      auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false,
-                                                 false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    }
-    const float mt = mx * c2;
-    const bool need = mt > m2 + kLazy;
-    if (__builtin_amdgcn_ballot_w64(need)) {
-      cold_path();
-      const float mnew = need ? mt : m2;
-      const float alpha = fast_exp2(m2 - mnew);
-      m2 = mnew;
-      l *= alpha;
-#pragma unroll
-      for (int c = 0; c < C::kCT; ++c) oacc[c] *= alpha;
-    }
-    float lsum = 0.f;
-    bf16x8 pf[C::kKSteps];
-#pragma unroll
-    for (int kt = 0; kt < C::kKTiles; ++kt) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         u32x4 w;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p0 = fast_exp2(__builtin_fmaf(sacc[kt][8 * h + 2 * e], c2, -m2));
-          const float p1 = fast_exp2(__builtin_fmaf(sacc[kt][8 * h + 2 * e + 1], c2, -m2));
-          lsum += p0 + p1;
+          const float p0 = fast_exp2(__builtin_fmaf(cur[kt][8 * h + 2 * e], c2, -m2));
+          const float p1 = fast_exp2(__builtin_fmaf(cur[kt][8 * h + 2 * e + 1], c2, -m2));
+          la += p0;
+          lb += p1;
           w[e] = pack_bf16x2(p0, p1);
         }
         pf[2 * kt + h] = __builtin_bit_cast(bf16x8, w);
       }
-    }
-    l += lsum;
-
-    // O^T += V^T P^T
+    lc += la + lb;
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-    for (int s = 0; s < C::kKSteps; ++s) {
+    for (int i = 0; i < C::kDSteps * C::kKTiles; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // O += V_j^T P_j on the matrix cores; row max of S_{j+1} on the ALU
+    const char* vbuf = lds_v + P * C::kTileBytes;
+#pragma unroll
+    for (int s = 0; s < C::kKSteps; ++s)
 #pragma unroll
       for (int c = 0; c < C::kCT; ++c) {
         const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (lds_bf16x4*)(vbuf + voff[0][c] + s * 16 * C::kRowBytes));
         const bf16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (lds_bf16x4*)(vbuf + voff[1][c] + s * 16 * C::kRowBytes));
-        const bf16x8 a = __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
-        oacc[c] = mfma32(a, pf[s], oacc[c]);
+        oacc[c] = mfma32(__builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7), pf[s], oacc[c]);
       }
+    {
+      float ma = -INFINITY, mb = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < C::kKTiles; ++kt)
+#pragma unroll
+        for (int rr = 0; rr < 16; rr += 2) {
+          ma = fmaxf(ma, nxt[kt][rr]);
+          mb = fmaxf(mb, nxt[kt][rr + 1]);
+        }
+      mx = fmaxf(ma, mb);
+      mx = max_halves(mx);
     }
-    // transposed V reads two MFMAs ahead
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-    for (int i = 0; i < C::kKSteps * C::kCT - 2; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    for (int i = 0; i < C::kKSteps * C::kCT; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
 
-    if (start + C::kBK >= hi) {
-      // end of chunk r: local result (loc_out_r, loc_lse_r), then the Eq. (5) merge
-      float lrow;
-      {
-        auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false,
-                                                   false);
-        lrow = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-      }
-      const float inv = 1.0f / lrow;
+    if (t0.start + C::kBK >= t0.hi) {
+      // end of chunk r0: loc_lse_r from the chunk's own row sum
+      const float lrow = sum_halves(lc);
       const float lse2r = m2 + fast_log2(lrow);
-      const int64_t qi = q0 + n;
       if constexpr (PARTIALS) {
+        const int64_t qi = q0 + n;
         if (qi < Nq) {
-          const int64_t row = ((int64_t)r * BH + bh) * Nq + qi;
+          const float inv = 1.0f / lrow;
+          const int64_t row = ((int64_t)r0 * BH + bh) * Nq + qi;
           float* po = part_out + row * D;
 #pragma unroll
           for (int c = 0; c < C::kCT; ++c)
@@ -344,43 +365,41 @@ __global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
             }
           if (g == 0) part_lse[row] = lse2r * kLn2;
         }
+#pragma unroll
+        for (int c = 0; c < C::kCT; ++c) oacc[c] = f32x16{};
+        m2 = -INFINITY;
       } else {
+        // Eq. (5) on the log-sum-exps; the numerator terms already share the reference m2
         const float M = fmaxf(lse2m, lse2r);
-        const float a = fast_exp2(lse2m - M);
-        const float b = fast_exp2(lse2r - M);
-        const float den = a + b;
-        const float wa = a / den;
-        const float wb = b * inv / den;
-#pragma unroll
-        for (int c = 0; c < C::kCT; ++c) om[c] = om[c] * wa + oacc[c] * wb;
-        lse2m = M + fast_log2(den);
+        lse2m = M + fast_log2(fast_exp2(lse2m - M) + fast_exp2(lse2r - M));
       }
-#pragma unroll
-      for (int c = 0; c < C::kCT; ++c) oacc[c] = f32x16{};
-      l = 0.f;
-      m2 = -INFINITY;
-      ++r;
+      lc = 0.f;
+      ++r0;
     }
+    t0 = t1;
+    t1 = t2;
+    t2 = walk.next<C::kBK>(t2);
+    return t0.start >= Nk;
+  };
 
-    if (!has_next) break;
-    wait_vmem_all();
-    __syncthreads();
-    cur ^= 1;
-    start = nstart;
-    hi = nhi;
+  while (true) {
+    if (step(sa, sb, std::integral_constant<int, 0>{})) break;
+    if (step(sb, sa, std::integral_constant<int, 1>{})) break;
   }
 
   if constexpr (!PARTIALS) {
     const int64_t qi = q0 + n;
     if (qi < Nq) {
+      // out = numerator / Eq. (5) denominator = oacc * 2^(m - lse)
+      const float f = fast_exp2(m2 - lse2m);
       __bf16* ob = out + (bh * Nq + qi) * D;
 #pragma unroll
       for (int c = 0; c < C::kCT; ++c)
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
           u32x2 w;
-          w[0] = pack_bf16x2(om[c][4 * rq], om[c][4 * rq + 1]);
-          w[1] = pack_bf16x2(om[c][4 * rq + 2], om[c][4 * rq + 3]);
+          w[0] = pack_bf16x2(oacc[c][4 * rq] * f, oacc[c][4 * rq + 1] * f);
+          w[1] = pack_bf16x2(oacc[c][4 * rq + 2] * f, oacc[c][4 * rq + 3] * f);
           *reinterpret_cast<u32x2*>(ob + c * 32 + 8 * rq + 4 * g) = w;
         }
       if (g == 0) lse[bh * Nq + qi] = lse2m * kLn2;

@@ -39,10 +39,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Value held by lane (l ^ 32), exchanged with v_permlane32_swap.
-__device__ __forceinline__ float swap_half(float x) {
+// x[l] + x[l ^ 32] and max(x[l], x[l ^ 32]) for every lane l, through v_permlane32_swap.  The
+// swap of two copies of x returns, for lanes below 32, (x[l], x[l + 32]) and for the others
+// (x[l - 32], x[l]): each result alone holds the lane's own value on one half of the wave, so the
+// two are always combined.
+__device__ __forceinline__ float sum_halves(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_halves(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // Logical workgroup id so that the workgroups resident on one XCD work on the same (b, h) slice.
