@@ -1,7 +1,7 @@
 // Recompute backward of ring-chunked attention, dQ part: bf16 MFMA with fp32 accumulation
 // (gfx950).
 //
-// Query-stationary, like the forward: one workgroup = 4 waves = one (b, h) and 128 queries (32
+// Query-stationary, like the forward: one workgroup = 8 waves = one (b, h) and 256 queries (32
 // per wave).  The key/value sequence is streamed chunk by chunk (ring steps, arXiv 2507.16697
 // Sec. III-A) in tiles of 64 keys that never straddle a chunk, double buffered in LDS and filled
 // by direct global->LDS loads one tile ahead.  dQ accumulates over every tile of every chunk in
@@ -24,8 +24,8 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 template <int D>
 struct DqCfg {
-  static constexpr int kThreads = 256;
-  static constexpr int kWaves = 4;
+  static constexpr int kThreads = 512;
+  static constexpr int kWaves = 8;
   static constexpr int kQW = 32;
   static constexpr int kBQ = kWaves * kQW;
   static constexpr int kBK = 64;                   // keys per tile
@@ -97,7 +97,7 @@ __device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(
+__global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse,
     const float* __restrict__ delta, float* __restrict__ dq, int BH, int64_t Nq, int64_t Nk,

@@ -1,6 +1,7 @@
 // Ring-chunked attention forward, bf16 storage, bf16 MFMA with fp32 accumulation (gfx950).
 //
-// One workgroup = 4 waves = one (b, h) and a tile of 128 queries (32 per wave).  The key/value
+// One workgroup = 8 waves (two per SIMD) = one (b, h) and a tile of 256 queries (32 per wave), so
+// that each K/V tile brought into LDS serves 256 queries.  The key/value
 // sequence is visited as R chunks (ring steps, arXiv 2507.16697 Sec. III-A), streamed through LDS
 // in tiles of 64 keys that never straddle a chunk boundary.  K and V tiles are double buffered
 // (the on-chip analogue of the paper's ping-pong buffers) and filled by direct global->LDS loads:
@@ -41,8 +42,8 @@ constexpr float kLazy = 8.0f;
 
 template <int D>
 struct FwdCfg {
-  static constexpr int kThreads = 256;
-  static constexpr int kWaves = 4;
+  static constexpr int kThreads = 512;
+  static constexpr int kWaves = 8;
   static constexpr int kQW = 32;                  // queries per wave
   static constexpr int kBQ = kWaves * kQW;        // queries per workgroup
   static constexpr int kBK = 64;                  // keys per tile
@@ -137,7 +138,7 @@ struct ChunkWalk {
 };
 
 template <int D, bool PARTIALS>
-__global__ __launch_bounds__(256, 2) void fwd_bf16_kernel(
+__global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     __bf16* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
     float* __restrict__ part_lse, int BH, int64_t Nq, int64_t Nk, int R, float c2) {
@@ -422,8 +423,9 @@ hipError_t launch(const FwdArgs& a) {
 }  // namespace
 
 int64_t fwd_bf16_workgroups(int64_t BH, int64_t Nq, int64_t d) {
-  const int64_t bq = 128;
   (void)d;
+  const int64_t bq = FwdCfg<128>::kBQ;
+  static_assert(FwdCfg<128>::kBQ == FwdCfg<64>::kBQ, "one query tile size");
   return BH * ((Nq + bq - 1) / bq);
 }
 
