@@ -107,6 +107,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8192)
     ap.add_argument("--no-merge", action="store_true")
+    ap.add_argument("--no-ring", action="store_true",
+                    help="skip the ring-step measurement (chunks arriving on a second stream)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -118,7 +120,7 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2507_16697_amd import inputs, ringx
+    from paper_2507_16697_amd import inputs, ring, ringx
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -259,6 +261,37 @@ def main():
                                                         kernel_source_hash(["merge.hip", "ringx_device.h"]))}
         log(f"[bench] lse_merge {mms:.3f} ms, {kernels['lse_merge']['GB/s']:.0f} GB/s")
         del part_out, part_lse
+
+    # the same step as R ring steps: every chunk arrives in a ping-pong buffer by a device copy on
+    # a second stream while the previous chunk is computed (ringx_attn_fwd_step / _bwd_step)
+    if not args.no_ring:
+        bounds = [ringx.ringx_chunk_bounds(Nk, R, r) for r in range(R)]
+        ks = [k[:, :, lo:hi].contiguous() for lo, hi in bounds]
+        vs = [v[:, :, lo:hi].contiguous() for lo, hi in bounds]
+
+        def ring_step():
+            o, l = ring.ring_forward(q, ks, vs, scale=w.scale)
+            ring.ring_backward(q, ks, vs, o, do, l, scale=w.scale)
+
+        ring_step()
+        torch.cuda.synchronize()
+        nr = max(1, min(K, 3))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(nr):
+            ring_step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        rms = e0.elapsed_time(e1) / nr
+        kernels["ring_steps"] = {
+            "ms": rms, "steps": nr, "chunks": R,
+            "tflops": 6 * U / (rms * 1e-3) / 1e12,
+            "overhead_vs_fused": rms / ms_step - 1.0,
+            "copied_bytes": 2 * B * H * Nk * d * 2 * 2,
+            "what": "fwd+bwd as R ring steps, chunk copies overlapped on a second stream",
+        }
+        log(f"[bench] ring steps: {rms:.2f} ms/step ({100 * (rms / ms_step - 1):+.1f}% vs fused)")
+        del ks, vs
 
     result = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,

@@ -140,6 +140,43 @@ ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, cons
                                int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
                                float scale, ringx_dtype dtype, hipStream_t stream);
 
+/*
+ * One ring step of the forward (Sec. III-A: at every step a GPU holds one K/V chunk of S/N tokens,
+ * computes its local result, and the results are merged by Eq. (5); "Communication and
+ * computation overlap": the next chunk arrives in a second buffer meanwhile).  Computes the local
+ * result (loc_out, loc_lse) of q against the one chunk k, v [B,H,Nk,d] (Nk = the chunk's length)
+ * and folds it into the running result by Eq. (5):
+ *   M = max(lse_acc, loc_lse);  a = exp(lse_acc - M);  b = exp(loc_lse - M);
+ *   out_acc <- (a out_acc + b loc_out) / (a + b);  lse_acc <- M + log(a + b).
+ *   out_acc [B,H,Nq,d] fp32, lse_acc [B,H,Nq] fp32 -- caller-owned, read and written in place
+ *   (normalised output and natural-log lse of every chunk merged so far).
+ *   first != 0: the accumulator holds nothing yet; it is overwritten (its contents are ignored).
+ * After the last step, ringx_lse_merge with R = 1 turns (out_acc, lse_acc) into the output dtype.
+ * Steps on one accumulator must be ordered (same stream or synchronised); the chunks may come in
+ * any order (the merge is exact up to rounding).
+ */
+ringx_status ringx_attn_fwd_step(const void* q, const void* k, const void* v, float* out_acc,
+                                 float* lse_acc, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
+                                 int64_t d, float scale, ringx_dtype dtype, int first,
+                                 hipStream_t stream);
+
+/*
+ * One ring step of the backward (Sec. III-A, "Communication scheme": the K/V chunk's gradients
+ * are computed at the step that holds the chunk and sent back to its owner; dQ accumulates over
+ * the N steps).  With lse and delta of the whole sequence (the merged lse, D from
+ * ringx_bwd_preprocess), for the one chunk k, v [B,H,Nk,d]:
+ *   dk, dv [B,H,Nk,d] fp32 -- the chunk's gradients, overwritten or added to
+ *   (accumulate_dkv != 0);
+ *   dq_acc [B,H,Nq,d] fp32 -- the chunk's contribution to dQ, added to the running sum
+ *   (accumulate_dq != 0) or overwriting it (the first step).
+ * Steps that touch one dq_acc must be ordered.
+ */
+ringx_status ringx_attn_bwd_step(const void* q, const void* k, const void* v, const void* dout,
+                                 const float* lse, const float* delta, float* dq_acc, float* dk,
+                                 float* dv, int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
+                                 float scale, ringx_dtype dtype, int accumulate_dq,
+                                 int accumulate_dkv, hipStream_t stream);
+
 /* Bytes of backward workspace for these arguments (0 if the arguments are invalid).  Host only. */
 size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
                                  int64_t R, ringx_dtype dtype);

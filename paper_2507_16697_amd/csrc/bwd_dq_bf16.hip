@@ -101,7 +101,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse,
     const float* __restrict__ delta, float* __restrict__ dq, int BH, int64_t Nq, int64_t Nk,
-    int R, float c2, float scale) {
+    int R, float c2, float scale, int accumulate) {
   using C = DqCfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds_k[2 * C::kTileBytes];
   __shared__ __attribute__((aligned(1024))) char lds_v[2 * C::kTileBytes];
@@ -274,7 +274,9 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
       for (int rq = 0; rq < 4; ++rq) {
         f32x4 val = {dqacc[c][4 * rq] * scale, dqacc[c][4 * rq + 1] * scale,
                      dqacc[c][4 * rq + 2] * scale, dqacc[c][4 * rq + 3] * scale};
-        *reinterpret_cast<f32x4*>(dqr + c * 32 + 8 * rq + 4 * g) = val;
+        f32x4* dst = reinterpret_cast<f32x4*>(dqr + c * 32 + 8 * rq + 4 * g);
+        if (accumulate) val += *dst;
+        *dst = val;
       }
   }
 }
@@ -287,7 +289,7 @@ hipError_t launch(const BwdArgs& a) {
   hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
                      (const __bf16*)a.dout, a.lse, a.delta, a.dq, (int)a.BH, a.Nq, a.Nk,
-                     (int)a.R, a.scale * kLog2e, a.scale);
+                     (int)a.R, a.scale * kLog2e, a.scale, a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -61,7 +61,7 @@ template <int DMAX>
 __global__ __launch_bounds__(kThreads) void bwd_f32_dq_kernel(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     const float* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    float* __restrict__ dq, int64_t Nq, int64_t Nk, int d, float scale) {
+    float* __restrict__ dq, int64_t Nq, int64_t Nk, int d, float scale, int accumulate) {
   const int64_t bh = blockIdx.y;
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (i >= Nq) return;
@@ -91,7 +91,10 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_dq_kernel(
   }
 #pragma unroll
   for (int c = 0; c < DMAX; ++c)
-    if (c < d) dq[(bh * Nq + i) * d + c] = gq[c] * scale;
+    if (c < d) {
+      float* dst = dq + (bh * Nq + i) * d + c;
+      *dst = (accumulate ? *dst : 0.f) + gq[c] * scale;
+    }
 }
 
 template <int DMAX>
@@ -109,7 +112,8 @@ hipError_t launch_dq(const BwdArgs& a) {
   const dim3 gq((uint32_t)((a.Nq + kThreads - 1) / kThreads), (uint32_t)a.BH);
   hipLaunchKernelGGL((bwd_f32_dq_kernel<DMAX>), gq, dim3(kThreads), 0, a.stream,
                      (const float*)a.q, (const float*)a.k, (const float*)a.v,
-                     (const float*)a.dout, a.lse, a.delta, a.dq, a.Nq, a.Nk, (int)a.d, a.scale);
+                     (const float*)a.dout, a.lse, a.delta, a.dq, a.Nq, a.Nk, (int)a.d, a.scale,
+                     a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -25,8 +25,9 @@
 // merged lse by Eq. (5).  The output numerator is kept unnormalised: Eq. (5)'s term
 // exp(loc_lse_r - M) loc_out_r equals exp(m - M) times the chunk's unnormalised accumulator, so
 // one accumulator holds the running sum of all chunk terms and the final division by the Eq. (5)
-// denominator is a multiplication by 2^(m - lse).  PARTIALS = true instead writes every chunk's
-// (loc_out_r, loc_lse_r) and restarts the accumulator.
+// denominator is a multiplication by 2^(m - lse).  MODE kPartials instead writes every chunk's
+// (loc_out_r, loc_lse_r) and restarts the accumulator; MODE kStep (one chunk, R = 1) merges the
+// chunk's result into a running fp32 (acc_out, acc_lse) by Eq. (5), one ring step at a time.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
@@ -137,12 +138,15 @@ struct ChunkWalk {
   }
 };
 
-template <int D, bool PARTIALS>
+template <int D, int MODE>
 __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     __bf16* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
-    float* __restrict__ part_lse, int BH, int64_t Nq, int64_t Nk, int R, float c2) {
+    float* __restrict__ part_lse, float* __restrict__ acc_out, float* __restrict__ acc_lse,
+    int first, int BH, int64_t Nq, int64_t Nk, int R, float c2) {
   using C = FwdCfg<D>;
+  constexpr bool kPartials = MODE == (int)FwdMode::kPartials;
+  constexpr bool kStep = MODE == (int)FwdMode::kStep;
   __shared__ __attribute__((aligned(1024))) char lds_k[2 * C::kTileBytes];
   __shared__ __attribute__((aligned(1024))) char lds_v[2 * C::kTileBytes];
 
@@ -350,7 +354,42 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
       // end of chunk r0: loc_lse_r from the chunk's own row sum
       const float lrow = sum_halves(lc);
       const float lse2r = m2 + fast_log2(lrow);
-      if constexpr (PARTIALS) {
+      if constexpr (kStep) {
+        // Eq. (5) with the running result: out_acc <- (out_acc a + loc_out b) / (a + b)
+        const int64_t qi = q0 + n;
+        if (qi < Nq) {
+          const int64_t row = bh * Nq + qi;
+          float* ao = acc_out + row * D;
+          const float inv = 1.0f / lrow;
+          float wa = 0.f, wb = inv;
+          float lnew = lse2r;
+          if (!first) {
+            const float lold = acc_lse[row] * kLog2e;
+            const float M = fmaxf(lold, lse2r);
+            const float a = fast_exp2(lold - M);
+            const float b = fast_exp2(lse2r - M);
+            const float den = a + b;
+            wa = a / den;
+            wb = b * inv / den;
+            lnew = M + fast_log2(den);
+          }
+#pragma unroll
+          for (int c = 0; c < C::kCT; ++c)
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq) {
+              f32x4* dst = reinterpret_cast<f32x4*>(ao + c * 32 + 8 * rq + 4 * g);
+              const f32x4 prev = first ? f32x4{} : *dst;
+              f32x4 val;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) val[e] = prev[e] * wa + oacc[c][4 * rq + e] * wb;
+              *dst = val;
+            }
+          if (g == 0) acc_lse[row] = lnew * kLn2;
+        }
+#pragma unroll
+        for (int c = 0; c < C::kCT; ++c) oacc[c] = f32x16{};
+        m2 = -INFINITY;
+      } else if constexpr (kPartials) {
         const int64_t qi = q0 + n;
         if (qi < Nq) {
           const float inv = 1.0f / lrow;
@@ -388,7 +427,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     if (step(sb, sa, std::integral_constant<int, 1>{})) break;
   }
 
-  if constexpr (!PARTIALS) {
+  if constexpr (MODE == (int)FwdMode::kFused) {
     const int64_t qi = q0 + n;
     if (qi < Nq) {
       // out = numerator / Eq. (5) denominator = oacc * 2^(m - lse)
@@ -408,16 +447,25 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
   }
 }
 
-template <int D, bool PARTIALS>
+template <int D, int MODE>
 hipError_t launch(const FwdArgs& a) {
   using C = FwdCfg<D>;
   const int64_t nqt = (a.Nq + C::kBQ - 1) / C::kBQ;
   const int64_t nwg = nqt * a.BH;
-  hipLaunchKernelGGL((fwd_bf16_kernel<D, PARTIALS>), dim3((uint32_t)nwg), dim3(C::kThreads), 0,
+  hipLaunchKernelGGL((fwd_bf16_kernel<D, MODE>), dim3((uint32_t)nwg), dim3(C::kThreads), 0,
                      a.stream, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (__bf16*)a.out, a.lse, a.part_out, a.part_lse, (int)a.BH, a.Nq, a.Nk,
-                     (int)a.R, a.scale * kLog2e);
+                     (__bf16*)a.out, a.lse, a.part_out, a.part_lse, a.acc_out, a.acc_lse,
+                     a.first ? 1 : 0, (int)a.BH, a.Nq, a.Nk, (int)a.R, a.scale * kLog2e);
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_mode(const FwdArgs& a, FwdMode mode) {
+  switch (mode) {
+    case FwdMode::kPartials: return launch<D, (int)FwdMode::kPartials>(a);
+    case FwdMode::kStep: return launch<D, (int)FwdMode::kStep>(a);
+    default: return launch<D, (int)FwdMode::kFused>(a);
+  }
 }
 
 }  // namespace
@@ -429,9 +477,8 @@ int64_t fwd_bf16_workgroups(int64_t BH, int64_t Nq, int64_t d) {
   return BH * ((Nq + bq - 1) / bq);
 }
 
-hipError_t launch_fwd_bf16(const FwdArgs& a, bool partials) {
-  if (a.d == 128) return partials ? launch<128, true>(a) : launch<128, false>(a);
-  return partials ? launch<64, true>(a) : launch<64, false>(a);
+hipError_t launch_fwd_bf16(const FwdArgs& a, FwdMode mode) {
+  return a.d == 128 ? launch_mode<128>(a, mode) : launch_mode<64>(a, mode);
 }
 
 }  // namespace ringx

@@ -4,7 +4,8 @@
 // every chunk r the thread runs an online softmax over the chunk's keys (Eqs. (2)-(4) of arXiv
 // 2507.16697 Sec. III-A), forms the chunk's local result (loc_out_r, loc_lse_r), and either writes
 // it (partials mode) or folds it into the Eq. (5) merge.  The merged output accumulates in place in
-// the fp32 output row, which only this thread touches.
+// the fp32 output row, which only this thread touches.  Step mode (R = 1) folds the one chunk into
+// a running fp32 (acc_out, acc_lse) left by earlier ring steps.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
@@ -15,11 +16,14 @@ namespace {
 constexpr int kF32Threads = 128;
 constexpr int kF32Tile = 32;
 
-template <int DMAX, bool PARTIALS>
+template <int DMAX, int MODE>
 __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     float* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
-    float* __restrict__ part_lse, int64_t BH, int64_t Nq, int64_t Nk, int R, int d, float scale) {
+    float* __restrict__ part_lse, float* __restrict__ acc_out, float* __restrict__ acc_lse,
+    int first, int64_t BH, int64_t Nq, int64_t Nk, int R, int d, float scale) {
+  constexpr bool PARTIALS = MODE == (int)FwdMode::kPartials;
+  constexpr bool STEP = MODE == (int)FwdMode::kStep;
   __shared__ float ks[kF32Tile * DMAX];
   __shared__ float vs[kF32Tile * DMAX];
   const int t = threadIdx.x;
@@ -32,9 +36,10 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
   float qr[DMAX];
 #pragma unroll
   for (int c = 0; c < DMAX; ++c) qr[c] = (active && c < d) ? q[(bh * Nq + qi) * d + c] : 0.f;
-  float* orow = out + (bh * Nq + (active ? qi : 0)) * d;
+  float* orow = (STEP ? acc_out : out) + (bh * Nq + (active ? qi : 0)) * d;
+  // step mode starts from the running result of the earlier ring steps
+  float lse_m = (STEP && !first && active) ? acc_lse[bh * Nq + qi] : -INFINITY;
 
-  float lse_m = -INFINITY;
   for (int r = 0; r < R; ++r) {
     const int64_t lo = (int64_t)r * Nk / R;
     const int64_t hi = (int64_t)(r + 1) * Nk / R;
@@ -85,37 +90,40 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
       const float wb = b * inv / den;
 #pragma unroll
       for (int c = 0; c < DMAX; ++c)
-        if (c < d) orow[c] = (r == 0 ? 0.f : orow[c] * wa) + o[c] * wb;
+        if (c < d) orow[c] = (lse_m == -INFINITY ? 0.f : orow[c] * wa) + o[c] * wb;
       lse_m = M + logf(den);
     }
   }
   if constexpr (!PARTIALS) {
-    if (active) lse[bh * Nq + qi] = lse_m;
+    if (active) (STEP ? acc_lse : lse)[bh * Nq + qi] = lse_m;
   }
 }
 
-template <int DMAX>
-hipError_t launch(const FwdArgs& a, bool partials) {
+template <int DMAX, int MODE>
+hipError_t launch(const FwdArgs& a) {
   dim3 grid((uint32_t)((a.Nq + kF32Threads - 1) / kF32Threads), (uint32_t)a.BH);
-  if (partials)
-    hipLaunchKernelGGL((fwd_f32_kernel<DMAX, true>), grid, dim3(kF32Threads), 0, a.stream,
-                       (const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.out,
-                       a.lse, a.part_out, a.part_lse, a.BH, a.Nq, a.Nk, (int)a.R, (int)a.d,
-                       a.scale);
-  else
-    hipLaunchKernelGGL((fwd_f32_kernel<DMAX, false>), grid, dim3(kF32Threads), 0, a.stream,
-                       (const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.out,
-                       a.lse, a.part_out, a.part_lse, a.BH, a.Nq, a.Nk, (int)a.R, (int)a.d,
-                       a.scale);
+  hipLaunchKernelGGL((fwd_f32_kernel<DMAX, MODE>), grid, dim3(kF32Threads), 0, a.stream,
+                     (const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.out,
+                     a.lse, a.part_out, a.part_lse, a.acc_out, a.acc_lse, a.first ? 1 : 0, a.BH,
+                     a.Nq, a.Nk, (int)a.R, (int)a.d, a.scale);
   return hipGetLastError();
+}
+
+template <int DMAX>
+hipError_t launch_mode(const FwdArgs& a, FwdMode mode) {
+  switch (mode) {
+    case FwdMode::kPartials: return launch<DMAX, (int)FwdMode::kPartials>(a);
+    case FwdMode::kStep: return launch<DMAX, (int)FwdMode::kStep>(a);
+    default: return launch<DMAX, (int)FwdMode::kFused>(a);
+  }
 }
 
 }  // namespace
 
-hipError_t launch_fwd_f32(const FwdArgs& a, bool partials) {
-  if (a.d <= 32) return launch<32>(a, partials);
-  if (a.d <= 64) return launch<64>(a, partials);
-  return launch<128>(a, partials);
+hipError_t launch_fwd_f32(const FwdArgs& a, FwdMode mode) {
+  if (a.d <= 32) return launch_mode<32>(a, mode);
+  if (a.d <= 64) return launch_mode<64>(a, mode);
+  return launch_mode<128>(a, mode);
 }
 
 }  // namespace ringx

@@ -109,9 +109,11 @@ ringx_status ringx_attn_fwd(const void* q, const void* k, const void* v, void* o
     for (Span i : {sq, sk, sv})
       if (overlap(o, i)) return RINGX_E_ALIAS;
   if (overlap(so, sl)) return RINGX_E_ALIAS;
-  ringx::FwdArgs a{q, k, v, out, lse, nullptr, nullptr, bh, Nq, Nk, d, R, scale, stream};
-  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, false)
-                                        : ringx::launch_fwd_f32(a, false));
+  ringx::FwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.out = out, a.lse = lse;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, ringx::FwdMode::kFused)
+                                        : ringx::launch_fwd_f32(a, ringx::FwdMode::kFused));
 }
 
 ringx_status ringx_attn_fwd_partials(const void* q, const void* k, const void* v, float* part_out,
@@ -132,9 +134,11 @@ ringx_status ringx_attn_fwd_partials(const void* q, const void* k, const void* v
     for (Span i : {sq, sk, sv})
       if (overlap(o, i)) return RINGX_E_ALIAS;
   if (overlap(so, sl)) return RINGX_E_ALIAS;
-  ringx::FwdArgs a{q, k, v, nullptr, nullptr, part_out, part_lse, bh, Nq, Nk, d, R, scale, stream};
-  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, true)
-                                        : ringx::launch_fwd_f32(a, true));
+  ringx::FwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.part_out = part_out, a.part_lse = part_lse;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, ringx::FwdMode::kPartials)
+                                        : ringx::launch_fwd_f32(a, ringx::FwdMode::kPartials));
 }
 
 ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void* out, float* lse,
@@ -157,7 +161,9 @@ ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void*
     for (Span i : {si, sil})
       if (overlap(o, i)) return RINGX_E_ALIAS;
   if (overlap(so, sl)) return RINGX_E_ALIAS;
-  ringx::MergeArgs a{part_out, part_lse, out, lse, R, bh, Nq, d, out_dtype == RINGX_BF16, stream};
+  ringx::MergeArgs a;
+  a.part_out = part_out, a.part_lse = part_lse, a.out = out, a.lse = lse;
+  a.R = R, a.BH = bh, a.Nq = Nq, a.d = d, a.out_bf16 = out_dtype == RINGX_BF16, a.stream = stream;
   return hip_status(ringx::launch_lse_merge(a));
 }
 
@@ -174,8 +180,9 @@ ringx_status ringx_bwd_preprocess(const void* out, const void* dout, float* delt
   const Span sd = span(delta, bh * Nq * 4);
   if (overlap(sd, span(out, bh * Nq * d * es)) || overlap(sd, span(dout, bh * Nq * d * es)))
     return RINGX_E_ALIAS;
-  ringx::BwdArgs a{nullptr, nullptr, nullptr, out, dout, nullptr, nullptr, nullptr, nullptr,
-                   delta, bh, Nq, 1, d, 1, 1.0f, false, stream};
+  ringx::BwdArgs a;
+  a.out = out, a.dout = dout, a.delta = delta;
+  a.BH = bh, a.Nq = Nq, a.Nk = 1, a.d = d, a.R = 1, a.stream = stream;
   return hip_status(ringx::launch_bwd_pre(a, dtype == RINGX_BF16));
 }
 
@@ -219,8 +226,11 @@ ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
                                     {span(dk, bh * Nk * d * 4), span(dv, bh * Nk * d * 4)}, B, H,
                                     Nq, Nk, d, R, scale, dtype);
   if (st != RINGX_OK) return st;
-  ringx::BwdArgs a{q,  k,  v,  nullptr, dout, lse,   nullptr, dk, dv, const_cast<float*>(delta),
-                   bh, Nq, Nk, d,       R,    scale, accumulate_dkv != 0, stream};
+  ringx::BwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.dk = dk, a.dv = dv;
+  a.delta = const_cast<float*>(delta);
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale;
+  a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dkdv_bf16(a)
                                         : ringx::launch_bwd_dkdv_f32(a));
 }
@@ -234,8 +244,10 @@ ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, cons
   ringx_status st = check_bwd_stage(q, k, v, dout, lse, delta, {span(dq, bh * Nq * d * 4)}, B, H,
                                     Nq, Nk, d, R, scale, dtype);
   if (st != RINGX_OK) return st;
-  ringx::BwdArgs a{q,  k,  v,  nullptr, dout, lse,   dq,    nullptr, nullptr,
-                   const_cast<float*>(delta), bh, Nq, Nk, d, R, scale, false, stream};
+  ringx::BwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.dq = dq;
+  a.delta = const_cast<float*>(delta);
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dq_bf16(a)
                                         : ringx::launch_bwd_dq_f32(a));
 }
@@ -273,8 +285,11 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
       if (overlap(outs[i], outs[j])) return RINGX_E_ALIAS;
   }
   float* delta = static_cast<float*>(workspace);
-  ringx::BwdArgs a{q,  k,  v,  out, dout, lse,   dq, dk, dv, delta,
-                   bh, Nq, Nk, d,   R,    scale, accumulate_dkv != 0, stream};
+  ringx::BwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.out = out, a.dout = dout, a.lse = lse;
+  a.dq = dq, a.dk = dk, a.dv = dv, a.delta = delta;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale;
+  a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
   const bool bf16 = dtype == RINGX_BF16;
   if (ringx::launch_bwd_pre(a, bf16) != hipSuccess) return RINGX_E_HIP;
   if ((bf16 ? ringx::launch_bwd_dkdv_bf16(a) : ringx::launch_bwd_dkdv_f32(a)) != hipSuccess)
@@ -282,4 +297,52 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
   return hip_status(bf16 ? ringx::launch_bwd_dq_bf16(a) : ringx::launch_bwd_dq_f32(a));
 }
 
+ringx_status ringx_attn_fwd_step(const void* q, const void* k, const void* v, float* out_acc,
+                                 float* lse_acc, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
+                                 int64_t d, float scale, ringx_dtype dtype, int first,
+                                 hipStream_t stream) {
+  if (!q || !k || !v || !out_acc || !lse_acc) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, 1, scale, dtype);
+  if (st != RINGX_OK) return st;
+  for (const void* p : {q, k, v, (const void*)out_acc, (const void*)lse_acc})
+    if (!aligned16(p)) return RINGX_E_ALIGN;
+  const int64_t es = esize(dtype), bh = B * H;
+  const Span sq = span(q, bh * Nq * d * es), sk = span(k, bh * Nk * d * es),
+             sv = span(v, bh * Nk * d * es);
+  const Span so = span(out_acc, bh * Nq * d * 4), sl = span(lse_acc, bh * Nq * 4);
+  for (Span o : {so, sl})
+    for (Span i : {sq, sk, sv})
+      if (overlap(o, i)) return RINGX_E_ALIAS;
+  if (overlap(so, sl)) return RINGX_E_ALIAS;
+  ringx::FwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.acc_out = out_acc, a.acc_lse = lse_acc, a.first = first != 0;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = 1, a.scale = scale, a.stream = stream;
+  return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, ringx::FwdMode::kStep)
+                                        : ringx::launch_fwd_f32(a, ringx::FwdMode::kStep));
+}
+
+ringx_status ringx_attn_bwd_step(const void* q, const void* k, const void* v, const void* dout,
+                                 const float* lse, const float* delta, float* dq_acc, float* dk,
+                                 float* dv, int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
+                                 float scale, ringx_dtype dtype, int accumulate_dq,
+                                 int accumulate_dkv, hipStream_t stream) {
+  if (!dq_acc || !dk || !dv) return RINGX_E_NULLPTR;
+  const int64_t bh = B * H;
+  ringx_status st = check_bwd_stage(
+      q, k, v, dout, lse, delta,
+      {span(dq_acc, bh * Nq * d * 4), span(dk, bh * Nk * d * 4), span(dv, bh * Nk * d * 4)}, B, H,
+      Nq, Nk, d, 1, scale, dtype);
+  if (st != RINGX_OK) return st;
+  ringx::BwdArgs a;
+  a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.delta = const_cast<float*>(delta);
+  a.dq = dq_acc, a.dk = dk, a.dv = dv;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = 1, a.scale = scale;
+  a.accumulate_dkv = accumulate_dkv != 0, a.accumulate_dq = accumulate_dq != 0, a.stream = stream;
+  const bool bf16 = dtype == RINGX_BF16;
+  if ((bf16 ? ringx::launch_bwd_dkdv_bf16(a) : ringx::launch_bwd_dkdv_f32(a)) != hipSuccess)
+    return RINGX_E_HIP;
+  return hip_status(bf16 ? ringx::launch_bwd_dq_bf16(a) : ringx::launch_bwd_dq_f32(a));
+}
+
 }  // extern "C"
+

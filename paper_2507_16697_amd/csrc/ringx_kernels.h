@@ -7,48 +7,59 @@
 
 namespace ringx {
 
+// What the forward does with each chunk's local result (loc_out_r, loc_lse_r).
+enum class FwdMode {
+  kFused = 0,     // Eq. (5) merge of all R chunks in registers -> out, lse
+  kPartials = 1,  // write every chunk's result -> part_out, part_lse
+  kStep = 2,      // R = 1: merge the one chunk into the running fp32 acc_out, acc_lse
+};
+
 struct FwdArgs {
-  const void* q;
-  const void* k;
-  const void* v;
-  void* out;          // merged output (fused mode)
-  float* lse;         // merged lse (fused mode)
-  float* part_out;    // [R,B,H,Nq,d] (partials mode)
-  float* part_lse;    // [R,B,H,Nq]   (partials mode)
-  int64_t BH, Nq, Nk, d, R;
-  float scale;
-  hipStream_t stream;
+  const void* q = nullptr;
+  const void* k = nullptr;
+  const void* v = nullptr;
+  void* out = nullptr;          // merged output (fused mode)
+  float* lse = nullptr;         // merged lse (fused mode)
+  float* part_out = nullptr;    // [R,B,H,Nq,d] (partials mode)
+  float* part_lse = nullptr;    // [R,B,H,Nq]   (partials mode)
+  float* acc_out = nullptr;     // [B,H,Nq,d] running merged output (step mode)
+  float* acc_lse = nullptr;     // [B,H,Nq]   running merged lse (step mode)
+  bool first = false;           // step mode: the accumulator holds nothing yet
+  int64_t BH = 0, Nq = 0, Nk = 0, d = 0, R = 1;
+  float scale = 1.f;
+  hipStream_t stream = nullptr;
 };
 
 struct MergeArgs {
-  const float* part_out;
-  const float* part_lse;
-  void* out;
-  float* lse;
-  int64_t R, BH, Nq, d;
-  bool out_bf16;
-  hipStream_t stream;
+  const float* part_out = nullptr;
+  const float* part_lse = nullptr;
+  void* out = nullptr;
+  float* lse = nullptr;
+  int64_t R = 1, BH = 0, Nq = 0, d = 0;
+  bool out_bf16 = false;
+  hipStream_t stream = nullptr;
 };
 
 struct BwdArgs {
-  const void* q;
-  const void* k;
-  const void* v;
-  const void* out;
-  const void* dout;
-  const float* lse;
-  float* dq;
-  float* dk;
-  float* dv;
-  float* delta;       // D_i = dout_i . out_i, [B,H,Nq]
-  int64_t BH, Nq, Nk, d, R;
-  float scale;
-  bool accumulate_dkv;
-  hipStream_t stream;
+  const void* q = nullptr;
+  const void* k = nullptr;
+  const void* v = nullptr;
+  const void* out = nullptr;
+  const void* dout = nullptr;
+  const float* lse = nullptr;
+  float* dq = nullptr;
+  float* dk = nullptr;
+  float* dv = nullptr;
+  float* delta = nullptr;       // D_i = dout_i . out_i, [B,H,Nq]
+  int64_t BH = 0, Nq = 0, Nk = 0, d = 0, R = 1;
+  float scale = 1.f;
+  bool accumulate_dkv = false;  // dk, dv += instead of =
+  bool accumulate_dq = false;   // dq += instead of =
+  hipStream_t stream = nullptr;
 };
 
-hipError_t launch_fwd_bf16(const FwdArgs& a, bool partials);
-hipError_t launch_fwd_f32(const FwdArgs& a, bool partials);
+hipError_t launch_fwd_bf16(const FwdArgs& a, FwdMode mode);
+hipError_t launch_fwd_f32(const FwdArgs& a, FwdMode mode);
 hipError_t launch_lse_merge(const MergeArgs& a);
 hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16);
 hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a);

@@ -7,6 +7,8 @@ supplies device memory and the current HIP stream.  Function names follow the C 
     part_out, part_lse = ringx_attn_fwd_partials(q, k, v, R)
     out, lse = ringx_lse_merge(part_out, part_lse, out_dtype=torch.bfloat16)
     dq, dk, dv = ringx_attn_bwd(q, k, v, out, dout, lse, R)
+    ringx_attn_fwd_step(q, k_r, v_r, out_acc, lse_acc, first=(r == 0))   # one ring step
+    ringx_attn_bwd_step(q, k_r, v_r, dout, lse, delta, dq_acc, dk_r, dv_r, accumulate_dq=(r > 0))
 
 The library must be built (``python -m paper_2507_16697_amd.build``); loading fails loudly if it
 is missing -- there is no fallback implementation.
@@ -31,7 +33,8 @@ STATUS_NAMES = {
 
 EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "ringx_attn_bwd",
             "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv", "ringx_attn_bwd_dq",
-            "ringx_bwd_workspace_bytes", "ringx_chunk_bounds", "ringx_status_str")
+            "ringx_attn_fwd_step", "ringx_attn_bwd_step", "ringx_bwd_workspace_bytes",
+            "ringx_chunk_bounds", "ringx_status_str")
 
 
 class RingxError(RuntimeError):
@@ -66,6 +69,11 @@ def lib() -> ctypes.CDLL:
                                           ctypes.c_float, ctypes.c_int, ctypes.c_int, _P]
         L.ringx_attn_bwd_dq.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                         ctypes.c_float, ctypes.c_int, _P]
+        L.ringx_attn_fwd_step.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, ctypes.c_float,
+                                          ctypes.c_int, ctypes.c_int, _P]
+        L.ringx_attn_bwd_step.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I,
+                                          ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_int, _P]
         L.ringx_bwd_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, ctypes.c_int]
         L.ringx_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.ringx_chunk_bounds.argtypes = [_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
@@ -73,7 +81,8 @@ def lib() -> ctypes.CDLL:
         L.ringx_status_str.restype = ctypes.c_char_p
         for name in ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge",
                      "ringx_attn_bwd", "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv",
-                     "ringx_attn_bwd_dq", "ringx_chunk_bounds"):
+                     "ringx_attn_bwd_dq", "ringx_attn_fwd_step", "ringx_attn_bwd_step",
+                     "ringx_chunk_bounds"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -267,3 +276,32 @@ def ringx_attn_bwd_dq(q, k, v, dout, lse, delta, R: int, scale=None, dq=None, st
                                  R, _scale(scale, d), _dtype_code(q), _stream(stream))
     _check("ringx_attn_bwd_dq", st)
     return dq
+
+
+def ringx_attn_fwd_step(q, k, v, out_acc, lse_acc, first: bool, scale=None, stream=None):
+    """One ring step: merge q's attention over the chunk k, v into the running fp32
+    (out_acc [B,H,Nq,d], lse_acc [B,H,Nq]) in place (Eq. (5)); first=True starts it."""
+    _dev(q, k, v, out_acc, lse_acc)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    st = lib().ringx_attn_fwd_step(q.data_ptr(), k.data_ptr(), v.data_ptr(), out_acc.data_ptr(),
+                                   lse_acc.data_ptr(), B, H, Nq, Nk, d, _scale(scale, d),
+                                   _dtype_code(q), 1 if first else 0, _stream(stream))
+    _check("ringx_attn_fwd_step", st)
+    return out_acc, lse_acc
+
+
+def ringx_attn_bwd_step(q, k, v, dout, lse, delta, dq_acc, dk, dv, accumulate_dq: bool,
+                        accumulate_dkv: bool = False, scale=None, stream=None):
+    """One ring step of the backward for the chunk k, v: its dk, dv (fp32, written or added to)
+    and its contribution to dq_acc (added to, or written when accumulate_dq is False)."""
+    _dev(q, k, v, dout, lse, delta, dq_acc, dk, dv)
+    B, H, Nq, d = q.shape
+    Nk = k.shape[2]
+    st = lib().ringx_attn_bwd_step(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
+                                   lse.data_ptr(), delta.data_ptr(), dq_acc.data_ptr(),
+                                   dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nk, d, _scale(scale, d),
+                                   _dtype_code(q), 1 if accumulate_dq else 0,
+                                   1 if accumulate_dkv else 0, _stream(stream))
+    _check("ringx_attn_bwd_step", st)
+    return dq_acc, dk, dv

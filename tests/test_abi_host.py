@@ -161,3 +161,29 @@ def test_gradient_stage_validation():
     assert dkdv(dv=OP + 8 * GB + 4) == ALIGN and dqs(dq=OP + 8) == ALIGN
     assert dkdv(dv=OP) == ALIAS and dkdv(dk=KP) == ALIAS and dqs(dq=LP) == ALIAS
     assert dqs(dq=LP + 8 * GB) == ALIAS    # dq over delta
+
+
+def fstep(q=QP, k=KP, v=VP, o=OP, l=LP, B=1, H=2, Nq=100, Nk=300, d=64, scale=0.125, dt=BF16,
+          first=1):
+    return ringx.lib().ringx_attn_fwd_step(q, k, v, o, l, B, H, Nq, Nk, d, scale, dt, first, None)
+
+
+def test_fwd_step_validation():
+    assert fstep(q=0) == NULLPTR and fstep(o=0) == NULLPTR and fstep(l=0) == NULLPTR
+    assert fstep(Nk=0) == SHAPE and fstep(scale=0.0) == SHAPE and fstep(B=0) == SHAPE
+    assert fstep(d=96) == UNSUP and fstep(dt=3) == UNSUP
+    assert fstep(o=OP + 4) == ALIGN and fstep(l=LP + 8) == ALIGN
+    assert fstep(o=QP) == ALIAS and fstep(l=VP) == ALIAS and fstep(l=OP) == ALIAS
+    assert fstep(B=1 << 20, H=1 << 20, Nq=1 << 20) == SHAPE
+
+
+def bstep(dq=OP, dk=OP + 8 * GB, dv=OP + 16 * GB, lse=LP, delta=LP + 8 * GB, d=64, Nk=300):
+    return ringx.lib().ringx_attn_bwd_step(QP, KP, VP, QP + 16 * GB, lse, delta, dq, dk, dv, 1, 2,
+                                           100, Nk, d, 0.125, BF16, 1, 0, None)
+
+
+def test_bwd_step_validation():
+    assert bstep(dq=0) == NULLPTR and bstep(dk=0) == NULLPTR and bstep(delta=0) == NULLPTR
+    assert bstep(Nk=0) == SHAPE and bstep(d=80) == UNSUP
+    assert bstep(dq=OP + 4) == ALIGN
+    assert bstep(dq=QP) == ALIAS and bstep(dk=OP) == ALIAS and bstep(dv=LP) == ALIAS

@@ -18,7 +18,8 @@ import torch
 import oracle
 from paper_2507_16697_amd import inputs, ringx
 
-from parity_util import TOL_BF16_LSE, TOL_BF16_REL_RMS, rel_rms_err, to_device, to_host_f64
+from parity_util import (TOL_BF16_LSE, TOL_BF16_REL_RMS, check_rows, rel_rms_err, to_device,
+                         to_host_f64)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -41,43 +42,6 @@ def _run(w, g, with_bwd=True):
     return res
 
 
-def _sample_rows(Nq):
-    """Rows at tile edges (query tiles of 128 and 64), the middle and the end."""
-    rows = {0, 1, 63, 64, 127, 128, 129, Nq // 2 - 1, Nq // 2 + 17, Nq - 129, Nq - 65, Nq - 2,
-            Nq - 1}
-    return np.array(sorted(r for r in rows if 0 <= r < Nq))
-
-
-def _check_rows(name, w, t, res, heads, with_bwd=True):
-    """out, lse (and dQ) of sampled rows of `heads` against the oracle, row by row."""
-    rows = _sample_rows(w.Nq)
-    got_o, ref_o, got_l, ref_l, got_dq, ref_dq = [], [], [], [], [], []
-    out = res["out"]
-    for h in heads:
-        q = inputs.to_f64(t["q"][0, h, rows], "bf16")
-        k = inputs.to_f64(t["k"][0, h], "bf16")
-        v = inputs.to_f64(t["v"][0, h], "bf16")
-        o, l = oracle.head_attention(q, k, v, w.scale)
-        got_o.append(to_host_f64(out[0, h, rows]))
-        ref_o.append(o)
-        got_l.append(to_host_f64(res["lse"][0, h, rows]))
-        ref_l.append(l)
-        if with_bwd:
-            do = inputs.to_f64(t["do"][0, h, rows], "bf16")
-            D = oracle.head_bwd_preprocess(o, do)
-            dq, _, _ = oracle.head_attention_bwd(q, k, v, do, l, D, w.scale)
-            got_dq.append(to_host_f64(res["dq"][0, h, rows]))
-            ref_dq.append(dq)
-    errs = {"out": rel_rms_err(np.concatenate(got_o), np.concatenate(ref_o)),
-            "lse": float(np.max(np.abs(np.concatenate(got_l) - np.concatenate(ref_l))))}
-    if with_bwd:
-        errs["dq"] = rel_rms_err(np.concatenate(got_dq), np.concatenate(ref_dq))
-    _report(f"{name} rows {list(rows)} heads {list(heads)}", **errs)
-    assert errs["out"] <= TOL_BF16_REL_RMS and errs["lse"] <= TOL_BF16_LSE
-    if with_bwd:
-        assert errs["dq"] <= TOL_BF16_REL_RMS
-
-
 def _check_invariants(name, g, res):
     dk, dv = res["dk"].double(), res["dv"].double()
     sdv, sdo = dv.sum(dim=2), g["do"].double().sum(dim=2)
@@ -97,7 +61,7 @@ def test_ring8_nk262k_d128_full_size():
     g = {key: to_device(val, "bf16") for key, val in t.items()}
     res = _run(w, g)
     _check_invariants(w.name, g, res)
-    _check_rows(w.name, w, t, res, heads=(0, 6, 15))
+    check_rows(w.name, w, t, res, heads=(0, 6, 15))
 
 
 def test_ring8_full_key_length_dkdv():
@@ -156,7 +120,7 @@ def test_turbulence_tokens_forward():
     g = {key: to_device(val, "bf16") for key, val in t.items()}
     res = _run(w, g, with_bwd=False)
     assert bool(torch.isfinite(res["out"].float()).all()) and bool(torch.isfinite(res["lse"]).all())
-    _check_rows(w.name, w, t, res, heads=(0, 3, 8, 15), with_bwd=False)
+    check_rows(w.name, w, t, res, heads=(0, 3, 8, 15), with_bwd=False)
 
 
 def test_long_nk524k_d128():
@@ -166,4 +130,4 @@ def test_long_nk524k_d128():
     g = {key: to_device(val, "bf16") for key, val in t.items()}
     res = _run(w, g)
     _check_invariants(w.name, g, res)
-    _check_rows(w.name, w, t, res, heads=(0, 15))
+    check_rows(w.name, w, t, res, heads=(0, 15))
