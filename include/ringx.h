@@ -177,6 +177,31 @@ ringx_status ringx_attn_bwd_step(const void* q, const void* k, const void* v, co
                                  float scale, ringx_dtype dtype, int accumulate_dq,
                                  int accumulate_dkv, hipStream_t stream);
 
+/*
+ * Grouped-query attention (Sec. VI lists RingX as compatible with GQA): Hkv K/V heads serve the H
+ * query heads, query head h reading K/V head h / (H / Hkv) (consecutive groups of G = H / Hkv;
+ * Hkv = H is ringx_attn_fwd, Hkv = 1 is multi-query attention).
+ *   q, out [B,H,Nq,d], k, v [B,Hkv,Nk,d] (dtype); lse [B,H,Nq] fp32.  Everything else as
+ *   ringx_attn_fwd.  RINGX_E_SHAPE if Hkv < 1 or Hkv does not divide H.
+ */
+ringx_status ringx_attn_fwd_gqa(const void* q, const void* k, const void* v, void* out,
+                                float* lse, int64_t B, int64_t H, int64_t Hkv, int64_t Nq,
+                                int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                hipStream_t stream);
+
+/*
+ * Backward of ringx_attn_fwd_gqa.  dq [B,H,Nq,d] fp32; dk, dv [B,Hkv,Nk,d] fp32 hold the sum of
+ * the gradients over the G query heads of each group (overwritten, or added to when
+ * accumulate_dkv != 0).  Workspace as ringx_attn_bwd (ringx_bwd_workspace_bytes with H query
+ * heads).  Everything else as ringx_attn_bwd.
+ */
+ringx_status ringx_attn_bwd_gqa(const void* q, const void* k, const void* v, const void* out,
+                                const void* dout, const float* lse, float* dq, float* dk,
+                                float* dv, int64_t B, int64_t H, int64_t Hkv, int64_t Nq,
+                                int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                int accumulate_dkv, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
 /* Bytes of backward workspace for these arguments (0 if the arguments are invalid).  Host only. */
 size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
                                  int64_t R, ringx_dtype dtype);

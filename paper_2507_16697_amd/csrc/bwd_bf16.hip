@@ -4,7 +4,8 @@
 // One workgroup = 8 waves = one (b, h) and a tile of 128 keys inside one chunk (a key tile never
 // straddles a chunk boundary).  With the merged log-sum-exp saved by the forward, every chunk's
 // gradients are independent (arXiv 2507.16697 Sec. III-A: K/V chunk gradients computed per
-// chunk), so the workgroup sweeps every query tile of BQ queries once.  Wave w owns keys
+// chunk), so the workgroup sweeps every query tile of BQ queries once -- of every query head that
+// shares the K/V head when G > 1 query heads share one (grouped-query attention).  Wave w owns keys
 // 32*(w%4) .. +31 of the tile and query half w/4 of every query tile, and keeps fp32 dK^T, dV^T
 // accumulators for its keys in registers.  Per query tile:
 //   S   = Q K^T        A = Q rows (LDS),  B = K rows (LDS)              -> lane = key
@@ -109,7 +110,8 @@ template <int D>
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse,
-    const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BH,
+    const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BHkv,
+    int H, int grp,
     int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale, int accumulate) {
   using C = DkvCfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds[C::kLds];
@@ -125,22 +127,25 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 
   const uint32_t wg = xcd_remap(blockIdx.x, gridDim.x);
   const int64_t per_bh = (int64_t)R * tiles_per_chunk;
-  const int64_t bh = wg / per_bh;
+  const int64_t bh = wg / per_bh;   // K/V head (of B * H / G)
   const int r = (int)((wg % per_bh) / tiles_per_chunk);
   const int tile = (int)(wg % tiles_per_chunk);
-  if (bh >= BH) return;
+  if (bh >= BHkv) return;
   const int64_t lo = (int64_t)r * Nk / R;
   const int64_t hi = (int64_t)(r + 1) * Nk / R;
   const int64_t k0 = lo + (int64_t)tile * C::kBK;
   if (k0 >= hi) return;                         // uniform over the workgroup
   const int nvalid = (int)min<int64_t>(C::kBK, hi - k0);
 
-  const __bf16* qb = q + bh * Nq * D;
-  const __bf16* ob = dout + bh * Nq * D;
   const __bf16* kbp = k + bh * Nk * D;
   const __bf16* vbp = v + bh * Nk * D;
-  const float* lseb = lse + bh * Nq;
-  const float* deltab = delta + bh * Nq;
+  // the grp query heads sharing this K/V head are swept one after the other: query tile it is
+  // tile it % nqt of head qh0 + it / nqt
+  const int64_t qh0 = (bh / (H / grp)) * H + (bh % (H / grp)) * grp;
+  const __bf16* qb = q + qh0 * Nq * D;
+  const __bf16* ob = dout + qh0 * Nq * D;
+  const float* lseb = lse + qh0 * Nq;
+  const float* deltab = delta + qh0 * Nq;
 
   const int64_t nqt = (Nq + C::kBQ - 1) / C::kBQ;
 
@@ -187,18 +192,25 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   wait_vmem_all();
   __syncthreads();
 
-  for (int64_t it = 0; it < nqt; ++it) {
+  const int64_t ntiles = (int64_t)grp * nqt;
+  int64_t q0 = 0;     // first row of the current tile within its head
+  int64_t qn = 0;     // first row of the next tile, and the offset (in rows) of its head
+  int64_t hn = 0;
+  for (int64_t it = 0; it < ntiles; ++it) {
     const int cur = (int)(it & 1);
-    const int64_t q0 = it * C::kBQ;
     // next query tile in flight: Q, dO rows and their lse, D straight into LDS
-    if (it + 1 < nqt) {
-      const int64_t q1 = q0 + C::kBQ;
-      issue_rows<D>(qb, lbase + C::kOffQ + (cur ^ 1) * C::kQTile, q1, Nq - 1,
+    qn = q0 + C::kBQ;
+    if (qn >= Nq) {
+      qn = 0;
+      hn += Nq;
+    }
+    if (it + 1 < ntiles) {
+      issue_rows<D>(qb + hn * D, lbase + C::kOffQ + (cur ^ 1) * C::kQTile, qn, Nq - 1,
                     C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rows<D>(ob, lbase + C::kOffO + (cur ^ 1) * C::kQTile, q1, Nq - 1,
+      issue_rows<D>(ob + hn * D, lbase + C::kOffO + (cur ^ 1) * C::kQTile, qn, Nq - 1,
                     C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rowvals<C::kBQ>(lseb, deltab, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
-                            lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, q1, Nq - 1, wave, lane);
+      issue_rowvals<C::kBQ>(lseb + hn, deltab + hn, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
+                            lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, qn, Nq - 1, wave, lane);
     }
     // last query tile (rows past Nq are clamped copies) or a partial key tile
     const bool masked = q0 + C::kBQ > Nq || nvalid < C::kBK;
@@ -288,6 +300,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     // next tile landed (the only vector memory operations in flight); this tile's reads done
     wait_vmem_all();
     __syncthreads();
+    q0 = qn;
   }
 
   // the two query halves of a key block add their dK^T / dV^T through LDS
@@ -334,10 +347,11 @@ hipError_t launch(const BwdArgs& a) {
   using C = DkvCfg<D>;
   const int64_t max_chunk = (a.Nk + a.R - 1) / a.R;
   const int64_t tpc = (max_chunk + C::kBK - 1) / C::kBK;
-  const int64_t nwg = a.BH * a.R * tpc;
+  const int64_t nwg = a.BH / a.G * a.R * tpc;
   hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (const __bf16*)a.dout, a.lse, a.delta, a.dk, a.dv, (int)a.BH, a.Nq, a.Nk,
+                     (const __bf16*)a.dout, a.lse, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
+                     (int)a.H, (int)a.G, a.Nq, a.Nk,
                      (int)a.R, (int)tpc, a.scale * kLog2e, a.scale, a.accumulate_dkv ? 1 : 0);
   return hipGetLastError();
 }

@@ -100,8 +100,8 @@ template <int D>
 __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse,
-    const float* __restrict__ delta, float* __restrict__ dq, int BH, int64_t Nq, int64_t Nk,
-    int R, float c2, float scale, int accumulate) {
+    const float* __restrict__ delta, float* __restrict__ dq, int BH, int H, int grp, int64_t Nq,
+    int64_t Nk, int R, float c2, float scale, int accumulate) {
   using C = DqCfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds_k[2 * C::kTileBytes];
   __shared__ __attribute__((aligned(1024))) char lds_v[2 * C::kTileBytes];
@@ -118,8 +118,9 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
   const int64_t q0 = (wg % nqt) * C::kBQ + wave * C::kQW;
   if (bh >= BH) return;
 
-  const char* kb = reinterpret_cast<const char*>(k + bh * Nk * D);
-  const char* vb = reinterpret_cast<const char*>(v + bh * Nk * D);
+  const int64_t kvh = kv_head(bh, H, grp);
+  const char* kb = reinterpret_cast<const char*>(k + kvh * Nk * D);
+  const char* vb = reinterpret_cast<const char*>(v + kvh * Nk * D);
   int goff[C::kLoads], grow[C::kLoads];
   load_offsets<D>(goff, grow, wave, lane);
 
@@ -288,7 +289,8 @@ hipError_t launch(const BwdArgs& a) {
   const int64_t nwg = nqt * a.BH;
   hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (const __bf16*)a.dout, a.lse, a.delta, a.dq, (int)a.BH, a.Nq, a.Nk,
+                     (const __bf16*)a.dout, a.lse, a.delta, a.dq, (int)a.BH, (int)a.H, (int)a.G,
+                     a.Nq, a.Nk,
                      (int)a.R, a.scale * kLog2e, a.scale, a.accumulate_dq ? 1 : 0);
   return hipGetLastError();
 }

@@ -1,7 +1,7 @@
 // Recompute backward in fp32 (storage and arithmetic), any head dim 1..128: the exactness path.
 //
-// Two plain kernels: one thread per key accumulates dK_j, dV_j over every query; one thread per
-// query accumulates dQ_i over every key.  Both recompute P_ij = exp(scale q_i.k_j - lse_i) from
+// Two plain kernels: one thread per key accumulates dK_j, dV_j over every query (of every query
+// head sharing the key's K/V head); one thread per query accumulates dQ_i over every key.  Both recompute P_ij = exp(scale q_i.k_j - lse_i) from
 // the merged log-sum-exp and dS_ij = P_ij (dout_i.v_j - D_i).
 
 #include "ringx_device.h"
@@ -17,8 +17,8 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_dkdv_kernel(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     const float* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
     float* __restrict__ dk, float* __restrict__ dv, int64_t Nq, int64_t Nk, int d, float scale,
-    int accumulate) {
-  const int64_t bh = blockIdx.y;
+    int accumulate, int H, int grp) {
+  const int64_t bh = blockIdx.y;   // K/V head (of B * H / G)
   const int64_t j = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (j >= Nk) return;
   float kr[DMAX], vr[DMAX], gk[DMAX], gv[DMAX];
@@ -29,24 +29,31 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_dkdv_kernel(
     gk[c] = 0.f;
     gv[c] = 0.f;
   }
-  const float* qb = q + bh * Nq * d;
-  const float* ob = dout + bh * Nq * d;
-  for (int64_t i = 0; i < Nq; ++i) {
-    float s = 0.f, dp = 0.f;
+  // the grp query heads sharing this K/V head each add their gradient contributions
+  const int hkv = H / grp;
+  const int64_t qh0 = (bh / hkv) * H + (bh % hkv) * grp;
+  for (int jh = 0; jh < grp; ++jh) {
+    const float* qb = q + (qh0 + jh) * Nq * d;
+    const float* ob = dout + (qh0 + jh) * Nq * d;
+    const float* lb = lse + (qh0 + jh) * Nq;
+    const float* db = delta + (qh0 + jh) * Nq;
+    for (int64_t i = 0; i < Nq; ++i) {
+      float s = 0.f, dp = 0.f;
 #pragma unroll
-    for (int c = 0; c < DMAX; ++c)
-      if (c < d) {
-        s = __builtin_fmaf(qb[i * d + c], kr[c], s);
-        dp = __builtin_fmaf(ob[i * d + c], vr[c], dp);
-      }
-    const float p = expf(s * scale - lse[bh * Nq + i]);
-    const float ds = p * (dp - delta[bh * Nq + i]);
+      for (int c = 0; c < DMAX; ++c)
+        if (c < d) {
+          s = __builtin_fmaf(qb[i * d + c], kr[c], s);
+          dp = __builtin_fmaf(ob[i * d + c], vr[c], dp);
+        }
+      const float p = expf(s * scale - lb[i]);
+      const float ds = p * (dp - db[i]);
 #pragma unroll
-    for (int c = 0; c < DMAX; ++c)
-      if (c < d) {
-        gv[c] = __builtin_fmaf(p, ob[i * d + c], gv[c]);
-        gk[c] = __builtin_fmaf(ds, qb[i * d + c], gk[c]);
-      }
+      for (int c = 0; c < DMAX; ++c)
+        if (c < d) {
+          gv[c] = __builtin_fmaf(p, ob[i * d + c], gv[c]);
+          gk[c] = __builtin_fmaf(ds, qb[i * d + c], gk[c]);
+        }
+    }
   }
 #pragma unroll
   for (int c = 0; c < DMAX; ++c)
@@ -61,7 +68,8 @@ template <int DMAX>
 __global__ __launch_bounds__(kThreads) void bwd_f32_dq_kernel(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     const float* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ delta,
-    float* __restrict__ dq, int64_t Nq, int64_t Nk, int d, float scale, int accumulate) {
+    float* __restrict__ dq, int64_t Nq, int64_t Nk, int d, float scale, int accumulate, int H,
+    int grp) {
   const int64_t bh = blockIdx.y;
   const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (i >= Nq) return;
@@ -74,8 +82,9 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_dq_kernel(
   }
   const float l = lse[bh * Nq + i];
   const float D = delta[bh * Nq + i];
-  const float* kb = k + bh * Nk * d;
-  const float* vb = v + bh * Nk * d;
+  const int64_t kvh = kv_head(bh, H, grp);
+  const float* kb = k + kvh * Nk * d;
+  const float* vb = v + kvh * Nk * d;
   for (int64_t j = 0; j < Nk; ++j) {
     float s = 0.f, dp = 0.f;
 #pragma unroll
@@ -99,11 +108,11 @@ __global__ __launch_bounds__(kThreads) void bwd_f32_dq_kernel(
 
 template <int DMAX>
 hipError_t launch_dkdv(const BwdArgs& a) {
-  const dim3 gk((uint32_t)((a.Nk + kThreads - 1) / kThreads), (uint32_t)a.BH);
+  const dim3 gk((uint32_t)((a.Nk + kThreads - 1) / kThreads), (uint32_t)(a.BH / a.G));
   hipLaunchKernelGGL((bwd_f32_dkdv_kernel<DMAX>), gk, dim3(kThreads), 0, a.stream,
                      (const float*)a.q, (const float*)a.k, (const float*)a.v,
                      (const float*)a.dout, a.lse, a.delta, a.dk, a.dv, a.Nq, a.Nk, (int)a.d,
-                     a.scale, a.accumulate_dkv ? 1 : 0);
+                     a.scale, a.accumulate_dkv ? 1 : 0, (int)a.H, (int)a.G);
   return hipGetLastError();
 }
 
@@ -113,7 +122,7 @@ hipError_t launch_dq(const BwdArgs& a) {
   hipLaunchKernelGGL((bwd_f32_dq_kernel<DMAX>), gq, dim3(kThreads), 0, a.stream,
                      (const float*)a.q, (const float*)a.k, (const float*)a.v,
                      (const float*)a.dout, a.lse, a.delta, a.dq, a.Nq, a.Nk, (int)a.d, a.scale,
-                     a.accumulate_dq ? 1 : 0);
+                     a.accumulate_dq ? 1 : 0, (int)a.H, (int)a.G);
   return hipGetLastError();
 }
 

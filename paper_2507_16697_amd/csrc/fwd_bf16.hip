@@ -143,7 +143,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     __bf16* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
     float* __restrict__ part_lse, float* __restrict__ acc_out, float* __restrict__ acc_lse,
-    int first, int BH, int64_t Nq, int64_t Nk, int R, float c2) {
+    int first, int BH, int H, int grp, int64_t Nq, int64_t Nk, int R, float c2) {
   using C = FwdCfg<D>;
   constexpr bool kPartials = MODE == (int)FwdMode::kPartials;
   constexpr bool kStep = MODE == (int)FwdMode::kStep;
@@ -163,8 +163,9 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
   if (bh >= BH) return;
 
   const __bf16* qb = q + bh * Nq * D;
-  const char* kb = reinterpret_cast<const char*>(k + bh * Nk * D);
-  const char* vb = reinterpret_cast<const char*>(v + bh * Nk * D);
+  const int64_t kvh = kv_head(bh, H, grp);
+  const char* kb = reinterpret_cast<const char*>(k + kvh * Nk * D);
+  const char* vb = reinterpret_cast<const char*>(v + kvh * Nk * D);
   int goff[C::kLoads], grow[C::kLoads];
   load_offsets<D>(goff, grow, wave, lane);
 
@@ -455,7 +456,8 @@ hipError_t launch(const FwdArgs& a) {
   hipLaunchKernelGGL((fwd_bf16_kernel<D, MODE>), dim3((uint32_t)nwg), dim3(C::kThreads), 0,
                      a.stream, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
                      (__bf16*)a.out, a.lse, a.part_out, a.part_lse, a.acc_out, a.acc_lse,
-                     a.first ? 1 : 0, (int)a.BH, a.Nq, a.Nk, (int)a.R, a.scale * kLog2e);
+                     a.first ? 1 : 0, (int)a.BH, (int)a.H, (int)a.G, a.Nq, a.Nk, (int)a.R,
+                     a.scale * kLog2e);
   return hipGetLastError();
 }
 

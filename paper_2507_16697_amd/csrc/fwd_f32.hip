@@ -21,7 +21,7 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     float* __restrict__ out, float* __restrict__ lse, float* __restrict__ part_out,
     float* __restrict__ part_lse, float* __restrict__ acc_out, float* __restrict__ acc_lse,
-    int first, int64_t BH, int64_t Nq, int64_t Nk, int R, int d, float scale) {
+    int first, int64_t BH, int H, int grp, int64_t Nq, int64_t Nk, int R, int d, float scale) {
   constexpr bool PARTIALS = MODE == (int)FwdMode::kPartials;
   constexpr bool STEP = MODE == (int)FwdMode::kStep;
   __shared__ float ks[kF32Tile * DMAX];
@@ -30,8 +30,9 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
   const int64_t bh = blockIdx.y;
   const int64_t qi = (int64_t)blockIdx.x * kF32Threads + t;
   const bool active = qi < Nq;
-  const float* kb = k + bh * Nk * d;
-  const float* vb = v + bh * Nk * d;
+  const int64_t kvh = kv_head(bh, H, grp);
+  const float* kb = k + kvh * Nk * d;
+  const float* vb = v + kvh * Nk * d;
 
   float qr[DMAX];
 #pragma unroll
@@ -105,7 +106,7 @@ hipError_t launch(const FwdArgs& a) {
   hipLaunchKernelGGL((fwd_f32_kernel<DMAX, MODE>), grid, dim3(kF32Threads), 0, a.stream,
                      (const float*)a.q, (const float*)a.k, (const float*)a.v, (float*)a.out,
                      a.lse, a.part_out, a.part_lse, a.acc_out, a.acc_lse, a.first ? 1 : 0, a.BH,
-                     a.Nq, a.Nk, (int)a.R, (int)a.d, a.scale);
+                     (int)a.H, (int)a.G, a.Nq, a.Nk, (int)a.R, (int)a.d, a.scale);
   return hipGetLastError();
 }
 

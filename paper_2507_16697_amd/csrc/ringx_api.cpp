@@ -93,17 +93,23 @@ ringx_status ringx_chunk_bounds(int64_t Nk, int64_t R, int64_t r, int64_t* lo, i
   return RINGX_OK;
 }
 
-ringx_status ringx_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
-                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
-                            float scale, ringx_dtype dtype, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Forward with Hkv K/V heads serving H query heads (Hkv divides H; Hkv = H is plain MHA).
+ringx_status fwd_impl(const void* q, const void* k, const void* v, void* out, float* lse,
+                      int64_t B, int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t d,
+                      int64_t R, float scale, ringx_dtype dtype, hipStream_t stream) {
   if (!q || !k || !v || !out || !lse) return RINGX_E_NULLPTR;
+  if (Hkv < 1 || H < 1 || H % Hkv != 0) return RINGX_E_SHAPE;
   ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
   if (st != RINGX_OK) return st;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) || !aligned16(lse))
     return RINGX_E_ALIGN;
-  const int64_t es = esize(dtype), bh = B * H;
-  const Span sq = span(q, bh * Nq * d * es), sk = span(k, bh * Nk * d * es),
-             sv = span(v, bh * Nk * d * es);
+  const int64_t es = esize(dtype), bh = B * H, bkv = B * Hkv;
+  const Span sq = span(q, bh * Nq * d * es), sk = span(k, bkv * Nk * d * es),
+             sv = span(v, bkv * Nk * d * es);
   const Span so = span(out, bh * Nq * d * es), sl = span(lse, bh * Nq * 4);
   for (Span o : {so, sl})
     for (Span i : {sq, sk, sv})
@@ -112,8 +118,26 @@ ringx_status ringx_attn_fwd(const void* q, const void* k, const void* v, void* o
   ringx::FwdArgs a;
   a.q = q, a.k = k, a.v = v, a.out = out, a.lse = lse;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
+  a.H = H, a.G = H / Hkv;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, ringx::FwdMode::kFused)
                                         : ringx::launch_fwd_f32(a, ringx::FwdMode::kFused));
+}
+
+}  // namespace
+
+extern "C" {
+
+ringx_status ringx_attn_fwd(const void* q, const void* k, const void* v, void* out, float* lse,
+                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                            float scale, ringx_dtype dtype, hipStream_t stream) {
+  return fwd_impl(q, k, v, out, lse, B, H, H, Nq, Nk, d, R, scale, dtype, stream);
+}
+
+ringx_status ringx_attn_fwd_gqa(const void* q, const void* k, const void* v, void* out,
+                                float* lse, int64_t B, int64_t H, int64_t Hkv, int64_t Nq,
+                                int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                hipStream_t stream) {
+  return fwd_impl(q, k, v, out, lse, B, H, Hkv, Nq, Nk, d, R, scale, dtype, stream);
 }
 
 ringx_status ringx_attn_fwd_partials(const void* q, const void* k, const void* v, float* part_out,
@@ -137,6 +161,7 @@ ringx_status ringx_attn_fwd_partials(const void* q, const void* k, const void* v
   ringx::FwdArgs a;
   a.q = q, a.k = k, a.v = v, a.part_out = part_out, a.part_lse = part_lse;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
+  a.H = H, a.G = 1;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, ringx::FwdMode::kPartials)
                                         : ringx::launch_fwd_f32(a, ringx::FwdMode::kPartials));
 }
@@ -182,7 +207,7 @@ ringx_status ringx_bwd_preprocess(const void* out, const void* dout, float* delt
     return RINGX_E_ALIAS;
   ringx::BwdArgs a;
   a.out = out, a.dout = dout, a.delta = delta;
-  a.BH = bh, a.Nq = Nq, a.Nk = 1, a.d = d, a.R = 1, a.stream = stream;
+  a.BH = bh, a.Nq = Nq, a.Nk = 1, a.d = d, a.R = 1, a.stream = stream, a.H = H, a.G = 1;
   return hip_status(ringx::launch_bwd_pre(a, dtype == RINGX_BF16));
 }
 
@@ -229,7 +254,7 @@ ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
   ringx::BwdArgs a;
   a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.dk = dk, a.dv = dv;
   a.delta = const_cast<float*>(delta);
-  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.H = H, a.G = 1;
   a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dkdv_bf16(a)
                                         : ringx::launch_bwd_dkdv_f32(a));
@@ -248,6 +273,7 @@ ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, cons
   a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.dq = dq;
   a.delta = const_cast<float*>(delta);
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
+  a.H = H, a.G = 1;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dq_bf16(a)
                                         : ringx::launch_bwd_dq_f32(a));
 }
@@ -259,12 +285,17 @@ size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, i
   return static_cast<size_t>((delta + 255) / 256 * 256);
 }
 
-ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const void* out,
-                            const void* dout, const float* lse, float* dq, float* dk, float* dv,
-                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
-                            float scale, ringx_dtype dtype, int accumulate_dkv, void* workspace,
-                            size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+ringx_status bwd_impl(const void* q, const void* k, const void* v, const void* out,
+                      const void* dout, const float* lse, float* dq, float* dk, float* dv,
+                      int64_t B, int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t d,
+                      int64_t R, float scale, ringx_dtype dtype, int accumulate_dkv,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv) return RINGX_E_NULLPTR;
+  if (Hkv < 1 || H < 1 || H % Hkv != 0) return RINGX_E_SHAPE;
   ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
   if (st != RINGX_OK) return st;
   const size_t need = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, dtype);
@@ -272,12 +303,12 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
   for (const void* p : {q, k, v, out, dout, (const void*)lse, (const void*)dq, (const void*)dk,
                         (const void*)dv, (const void*)workspace})
     if (!aligned16(p)) return RINGX_E_ALIGN;
-  const int64_t es = esize(dtype), bh = B * H;
-  const Span ins[] = {span(q, bh * Nq * d * es),    span(k, bh * Nk * d * es),
-                      span(v, bh * Nk * d * es),    span(out, bh * Nq * d * es),
+  const int64_t es = esize(dtype), bh = B * H, bkv = B * Hkv;
+  const Span ins[] = {span(q, bh * Nq * d * es),    span(k, bkv * Nk * d * es),
+                      span(v, bkv * Nk * d * es),   span(out, bh * Nq * d * es),
                       span(dout, bh * Nq * d * es), span(lse, bh * Nq * 4)};
-  const Span outs[] = {span(dq, bh * Nq * d * 4), span(dk, bh * Nk * d * 4),
-                       span(dv, bh * Nk * d * 4), span(workspace, (int64_t)need)};
+  const Span outs[] = {span(dq, bh * Nq * d * 4), span(dk, bkv * Nk * d * 4),
+                       span(dv, bkv * Nk * d * 4), span(workspace, (int64_t)need)};
   for (int i = 0; i < 4; ++i) {
     for (const Span& s : ins)
       if (overlap(outs[i], s)) return RINGX_E_ALIAS;
@@ -289,12 +320,36 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
   a.q = q, a.k = k, a.v = v, a.out = out, a.dout = dout, a.lse = lse;
   a.dq = dq, a.dk = dk, a.dv = dv, a.delta = delta;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale;
+  a.H = H, a.G = H / Hkv;
   a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
   const bool bf16 = dtype == RINGX_BF16;
   if (ringx::launch_bwd_pre(a, bf16) != hipSuccess) return RINGX_E_HIP;
   if ((bf16 ? ringx::launch_bwd_dkdv_bf16(a) : ringx::launch_bwd_dkdv_f32(a)) != hipSuccess)
     return RINGX_E_HIP;
   return hip_status(bf16 ? ringx::launch_bwd_dq_bf16(a) : ringx::launch_bwd_dq_f32(a));
+}
+
+}  // namespace
+
+extern "C" {
+
+ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const void* out,
+                            const void* dout, const float* lse, float* dq, float* dk, float* dv,
+                            int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                            float scale, ringx_dtype dtype, int accumulate_dkv, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream) {
+  return bwd_impl(q, k, v, out, dout, lse, dq, dk, dv, B, H, H, Nq, Nk, d, R, scale, dtype,
+                  accumulate_dkv, workspace, workspace_bytes, stream);
+}
+
+ringx_status ringx_attn_bwd_gqa(const void* q, const void* k, const void* v, const void* out,
+                                const void* dout, const float* lse, float* dq, float* dk,
+                                float* dv, int64_t B, int64_t H, int64_t Hkv, int64_t Nq,
+                                int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                int accumulate_dkv, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+  return bwd_impl(q, k, v, out, dout, lse, dq, dk, dv, B, H, Hkv, Nq, Nk, d, R, scale, dtype,
+                  accumulate_dkv, workspace, workspace_bytes, stream);
 }
 
 ringx_status ringx_attn_fwd_step(const void* q, const void* k, const void* v, float* out_acc,
@@ -317,6 +372,7 @@ ringx_status ringx_attn_fwd_step(const void* q, const void* k, const void* v, fl
   ringx::FwdArgs a;
   a.q = q, a.k = k, a.v = v, a.acc_out = out_acc, a.acc_lse = lse_acc, a.first = first != 0;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = 1, a.scale = scale, a.stream = stream;
+  a.H = H, a.G = 1;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_fwd_bf16(a, ringx::FwdMode::kStep)
                                         : ringx::launch_fwd_f32(a, ringx::FwdMode::kStep));
 }
@@ -336,7 +392,7 @@ ringx_status ringx_attn_bwd_step(const void* q, const void* k, const void* v, co
   ringx::BwdArgs a;
   a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.delta = const_cast<float*>(delta);
   a.dq = dq_acc, a.dk = dk, a.dv = dv;
-  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = 1, a.scale = scale;
+  a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = 1, a.scale = scale, a.H = H, a.G = 1;
   a.accumulate_dkv = accumulate_dkv != 0, a.accumulate_dq = accumulate_dq != 0, a.stream = stream;
   const bool bf16 = dtype == RINGX_BF16;
   if ((bf16 ? ringx::launch_bwd_dkdv_bf16(a) : ringx::launch_bwd_dkdv_f32(a)) != hipSuccess)

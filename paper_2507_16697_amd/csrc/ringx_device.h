@@ -52,6 +52,12 @@ __device__ __forceinline__ float max_halves(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// K/V head serving query head `bh` (of B*H): query heads come in consecutive groups of `grp` per
+// K/V head (grouped-query attention; grp = 1 is plain multi-head attention).
+__device__ __forceinline__ int64_t kv_head(int64_t bh, int H, int grp) {
+  return (bh / H) * (H / grp) + (bh % H) / grp;
+}
+
 // Logical workgroup id so that the workgroups resident on one XCD work on the same (b, h) slice.
 // The hardware hands consecutive workgroup ids to the 8 XCDs round robin; this groups id w's
 // XCD (w % 8) onto a contiguous range of logical ids.

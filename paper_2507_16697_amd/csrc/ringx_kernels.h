@@ -26,6 +26,7 @@ struct FwdArgs {
   float* acc_lse = nullptr;     // [B,H,Nq]   running merged lse (step mode)
   bool first = false;           // step mode: the accumulator holds nothing yet
   int64_t BH = 0, Nq = 0, Nk = 0, d = 0, R = 1;
+  int64_t H = 1, G = 1;         // query heads per batch; query heads per K/V head (GQA)
   float scale = 1.f;
   hipStream_t stream = nullptr;
 };
@@ -51,7 +52,8 @@ struct BwdArgs {
   float* dk = nullptr;
   float* dv = nullptr;
   float* delta = nullptr;       // D_i = dout_i . out_i, [B,H,Nq]
-  int64_t BH = 0, Nq = 0, Nk = 0, d = 0, R = 1;
+  int64_t BH = 0, Nq = 0, Nk = 0, d = 0, R = 1;   // BH = B * H query heads
+  int64_t H = 1, G = 1;         // query heads per batch; query heads per K/V head (GQA)
   float scale = 1.f;
   bool accumulate_dkv = false;  // dk, dv += instead of =
   bool accumulate_dq = false;   // dq += instead of =

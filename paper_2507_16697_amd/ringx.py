@@ -33,7 +33,8 @@ STATUS_NAMES = {
 
 EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "ringx_attn_bwd",
             "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv", "ringx_attn_bwd_dq",
-            "ringx_attn_fwd_step", "ringx_attn_bwd_step", "ringx_bwd_workspace_bytes",
+            "ringx_attn_fwd_step", "ringx_attn_bwd_step", "ringx_attn_fwd_gqa",
+            "ringx_attn_bwd_gqa", "ringx_bwd_workspace_bytes",
             "ringx_chunk_bounds", "ringx_status_str")
 
 
@@ -74,6 +75,11 @@ def lib() -> ctypes.CDLL:
         L.ringx_attn_bwd_step.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                           ctypes.c_float, ctypes.c_int, ctypes.c_int,
                                           ctypes.c_int, _P]
+        L.ringx_attn_fwd_gqa.argtypes = [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I,
+                                         ctypes.c_float, ctypes.c_int, _P]
+        L.ringx_attn_bwd_gqa.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I,
+                                         _I, _I, ctypes.c_float, ctypes.c_int, ctypes.c_int, _P,
+                                         ctypes.c_size_t, _P]
         L.ringx_bwd_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, ctypes.c_int]
         L.ringx_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.ringx_chunk_bounds.argtypes = [_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
@@ -82,7 +88,7 @@ def lib() -> ctypes.CDLL:
         for name in ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge",
                      "ringx_attn_bwd", "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv",
                      "ringx_attn_bwd_dq", "ringx_attn_fwd_step", "ringx_attn_bwd_step",
-                     "ringx_chunk_bounds"):
+                     "ringx_attn_fwd_gqa", "ringx_attn_bwd_gqa", "ringx_chunk_bounds"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -305,3 +311,44 @@ def ringx_attn_bwd_step(q, k, v, dout, lse, delta, dq_acc, dk, dv, accumulate_dq
                                    1 if accumulate_dkv else 0, _stream(stream))
     _check("ringx_attn_bwd_step", st)
     return dq_acc, dk, dv
+
+
+def ringx_attn_fwd_gqa(q, k, v, R: int, scale=None, out=None, lse=None, stream=None):
+    """Grouped-query attention: q [B,H,Nq,d], k, v [B,Hkv,Nk,d] with Hkv dividing H."""
+    torch = _torch()
+    _dev(q, k, v)
+    B, H, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
+    _dev(out, lse)
+    st = lib().ringx_attn_fwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                  lse.data_ptr(), B, H, Hkv, Nq, Nk, d, R, _scale(scale, d),
+                                  _dtype_code(q), _stream(stream))
+    _check("ringx_attn_fwd_gqa", st)
+    return out, lse
+
+
+def ringx_attn_bwd_gqa(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None, dv=None,
+                       accumulate_dkv=False, stream=None):
+    """Backward of ringx_attn_fwd_gqa: fp32 dq [B,H,Nq,d], dk, dv [B,Hkv,Nk,d] (group sums)."""
+    torch = _torch()
+    _dev(q, k, v, out, dout, lse)
+    B, H, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dq = torch.empty((B, H, Nq, d), **f32) if dq is None else dq
+    dk = torch.zeros((B, Hkv, Nk, d), **f32) if dk is None else dk
+    dv = torch.zeros((B, Hkv, Nk, d), **f32) if dv is None else dv
+    _dev(dq, dk, dv)
+    nbytes = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, _dtype_code(q))
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    st = lib().ringx_attn_bwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                  dout.data_ptr(), lse.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                  dv.data_ptr(), B, H, Hkv, Nq, Nk, d, R, _scale(scale, d),
+                                  _dtype_code(q), 1 if accumulate_dkv else 0, ws.data_ptr(),
+                                  ws.numel(), _stream(stream))
+    _check("ringx_attn_bwd_gqa", st)
+    return dq, dk, dv

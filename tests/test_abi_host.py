@@ -187,3 +187,21 @@ def test_bwd_step_validation():
     assert bstep(Nk=0) == SHAPE and bstep(d=80) == UNSUP
     assert bstep(dq=OP + 4) == ALIGN
     assert bstep(dq=QP) == ALIAS and bstep(dk=OP) == ALIAS and bstep(dv=LP) == ALIAS
+
+
+def test_gqa_validation():
+    L = ringx.lib()
+
+    def fwd_gqa(H=4, Hkv=2, q=QP, o=OP):
+        return L.ringx_attn_fwd_gqa(q, KP, VP, o, LP, 1, H, Hkv, 100, 300, 64, 3, 0.125, BF16,
+                                    None)
+
+    assert fwd_gqa(Hkv=3) == SHAPE and fwd_gqa(Hkv=0) == SHAPE and fwd_gqa(Hkv=8) == SHAPE
+    assert fwd_gqa(q=0) == NULLPTR and fwd_gqa(o=KP) == ALIAS
+
+    def bwd_gqa(Hkv=2, ws=VP + 32 * GB, wsb=1 << 20):
+        return L.ringx_attn_bwd_gqa(QP, KP, VP, QP + 8 * GB, QP + 16 * GB, LP, OP, OP + 8 * GB,
+                                    OP + 16 * GB, 1, 4, Hkv, 100, 300, 64, 3, 0.125, BF16, 0, ws,
+                                    wsb, None)
+
+    assert bwd_gqa(Hkv=3) == SHAPE and bwd_gqa(ws=0) == WORKSPACE
