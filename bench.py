@@ -107,6 +107,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8192)
     ap.add_argument("--no-merge", action="store_true")
+    ap.add_argument("--no-gqa", action="store_true",
+                    help="skip the grouped-query measurement (H/4 K/V heads)")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the ring-step measurement (chunks arriving on a second stream)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -292,6 +294,35 @@ def main():
         }
         log(f"[bench] ring steps: {rms:.2f} ms/step ({100 * (rms / ms_step - 1):+.1f}% vs fused)")
         del ks, vs
+
+    # grouped-query attention on the same shapes: H/4 K/V heads (the first H/4 heads of K and V)
+    if not args.no_gqa and H % 4 == 0:
+        hkv = H // 4
+        kg, vg = k[:, :hkv].contiguous(), v[:, :hkv].contiguous()
+        dkg = torch.empty((B, hkv, Nk, d), dtype=torch.float32, device=dev)
+        dvg = torch.empty_like(dkg)
+
+        def gqa_step():
+            o, l = ringx.ringx_attn_fwd_gqa(q, kg, vg, R, scale=w.scale, out=out, lse=lse,
+                                            stream=stream)
+            ringx.ringx_attn_bwd_gqa(q, kg, vg, o, do, l, R, scale=w.scale, dq=dq, dk=dkg,
+                                     dv=dvg, stream=stream)
+
+        gqa_step()
+        torch.cuda.synchronize()
+        ng = max(1, min(K, 3))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(ng):
+            gqa_step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        gms = e0.elapsed_time(e1) / ng
+        kernels["gqa_steps"] = {"ms": gms, "steps": ng, "H": H, "Hkv": hkv,
+                                "tflops": 6 * U / (gms * 1e-3) / 1e12,
+                                "what": "fwd+bwd with H/4 K/V heads (grouped-query attention)"}
+        log(f"[bench] gqa (Hkv={hkv}): {gms:.2f} ms/step, {6 * U / (gms * 1e-3) / 1e12:.1f} TFLOP/s")
+        del kg, vg, dkg, dvg
 
     result = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,

@@ -1,4 +1,5 @@
-"""fp64 CPU oracle for ring-chunked attention -- TEST INFRASTRUCTURE ONLY.
+"""fp64 CPU oracles for ring-chunked attention and the multi-fidelity tokenizer -- TEST
+INFRASTRUCTURE ONLY.
 
 Only the tests, the smoke check of the graft entry point and the benchmark's CPU-baseline leg may
 import this package.  The HIP product path never does, and the two share no code.
@@ -16,4 +17,12 @@ from .attention_fp64 import (  # noqa: F401
     head_partials,
     head_scores,
     lse_merge,
+)
+from .tokenizer_fp64 import (  # noqa: F401
+    crop,
+    gaussian_filter,
+    gaussian_weights,
+    mode_tokens,
+    patchify,
+    tt_tokenize,
 )
