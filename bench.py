@@ -107,6 +107,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8192)
     ap.add_argument("--no-merge", action="store_true")
+    ap.add_argument("--no-tokenizer", action="store_true",
+                    help="skip the multi-fidelity tokenizer measurement (1024^3 x 4 field)")
     ap.add_argument("--no-gqa", action="store_true",
                     help="skip the grouped-query measurement (H/4 K/V heads)")
     ap.add_argument("--no-ring", action="store_true",
@@ -323,6 +325,37 @@ def main():
                                 "what": "fwd+bwd with H/4 K/V heads (grouped-query attention)"}
         log(f"[bench] gqa (Hkv={hkv}): {gms:.2f} ms/step, {6 * U / (gms * 1e-3) / 1e12:.1f} TFLOP/s")
         del kg, vg, dkg, dvg
+
+    # multi-fidelity tokenizer: the three fidelity modes of Table III's (filter, ratio) pairs
+    # (1, 8x), (4, 2x), (8, 1x) with patch 1 over a DNS-sized 1024^3 x 4 fp32 field
+    if not args.no_tokenizer:
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(7)
+        C_, D_ = 4, 1024
+        field = torch.randn((C_, D_, D_, D_), device=dev, generator=gen)
+        modes = []
+        for k_, ratio in ((1, 8), (4, 2), (8, 1)):
+            centre = (D_ // 2, D_ // 3, D_ // 5)
+            tok = ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, stream=stream)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(5):
+                ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, tokens=tok, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            tms = e0.elapsed_time(e1) / 5
+            nbytes = C_ * (D_ // ratio) ** 3 * 4 + tok.numel() * 4
+            modes.append({"filter": k_, "ratio": ratio, "tokens": tok.shape[0], "ms": tms,
+                          "bytes": nbytes, "GB/s": nbytes / (tms * 1e-3) / 1e9,
+                          "frac": nbytes / (tms * 1e-3) / 1e9 / PEAK_HBM_GBS})
+            del tok
+        kernels["tt_tokenize"] = {"field": f"{C_}x{D_}^3 fp32", "patch": 1, "modes": modes,
+                                  "bound": "hbm"}
+        log("[bench] tokenizer: " + ", ".join(f"(k={m['filter']}, {m['ratio']}x) "
+                                              f"{m['ms']:.3f} ms {m['GB/s']:.0f} GB/s"
+                                              for m in modes))
+        del field
 
     result = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,

@@ -202,6 +202,26 @@ ringx_status ringx_attn_bwd_gqa(const void* q, const void* k, const void* v, con
                                 int accumulate_dkv, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
+/*
+ * One fidelity mode of the Turbulence Transformer's multi-fidelity input (Sec. III-B: the
+ * subdomain selection C_i, the Gaussian filter F_i of size k_i^3, the model's patches; Table III
+ * pairs filter k with mode-size ratio D/D_i), as tokens for the attention above:
+ *   field  [C, D, H, W] fp32 (x fastest) -- input, caller-owned device memory.
+ *   subdomain: D/ratio x H/ratio x W/ratio cells centred at (cz, cy, cx), taken periodically
+ *   (cells cz - (D/ratio)/2 ... along z, and likewise);
+ *   filter: weights w_i = exp(-(i - (k-1)/2)^2 / (2 sigma^2)) / sum, i < k (k <= 32), applied as
+ *   w_i w_j w_l over each k^3 window with stride k;
+ *   tokens [L, C p^3] in out_dtype (fp32 or bf16, round to nearest even) with
+ *   L = (D/(ratio k p)) (H/(ratio k p)) (W/(ratio k p)); token (pz, py, px) at px + Px (py + Py pz),
+ *   feature ((c p + iz) p + iy) p + ix.
+ * RINGX_E_SHAPE unless ratio divides D, H, W and k p divides each subdomain extent, the centre lies
+ * in the field and sigma is finite and > 0; RINGX_E_UNSUPPORTED for k > 32.
+ */
+ringx_status ringx_tt_tokenize(const float* field, void* tokens, int64_t C, int64_t D, int64_t H,
+                               int64_t W, int64_t k, int64_t ratio, int64_t cz, int64_t cy,
+                               int64_t cx, int64_t p, float sigma, ringx_dtype out_dtype,
+                               hipStream_t stream);
+
 /* Bytes of backward workspace for these arguments (0 if the arguments are invalid).  Host only. */
 size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
                                  int64_t R, ringx_dtype dtype);

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <climits>
 #include <initializer_list>
 
 #include "ringx.h"
@@ -400,5 +401,47 @@ ringx_status ringx_attn_bwd_step(const void* q, const void* k, const void* v, co
   return hip_status(bf16 ? ringx::launch_bwd_dq_bf16(a) : ringx::launch_bwd_dq_f32(a));
 }
 
+ringx_status ringx_tt_tokenize(const float* field, void* tokens, int64_t C, int64_t D, int64_t H,
+                               int64_t W, int64_t k, int64_t ratio, int64_t cz, int64_t cy,
+                               int64_t cx, int64_t p, float sigma, ringx_dtype out_dtype,
+                               hipStream_t stream) {
+  if (!field || !tokens) return RINGX_E_NULLPTR;
+  if (C < 1 || D < 1 || H < 1 || W < 1 || k < 1 || ratio < 1 || p < 1) return RINGX_E_SHAPE;
+  if (k > ringx::kMaxTokFilter) return RINGX_E_UNSUPPORTED;
+  if (out_dtype != RINGX_BF16 && out_dtype != RINGX_FP32) return RINGX_E_UNSUPPORTED;
+  if (!(std::isfinite(sigma) && sigma > 0.f)) return RINGX_E_SHAPE;
+  if (D % ratio || H % ratio || W % ratio) return RINGX_E_SHAPE;
+  const int64_t sz = D / ratio, sy = H / ratio, sx = W / ratio;   // subdomain
+  if (sz % (k * p) || sy % (k * p) || sx % (k * p)) return RINGX_E_SHAPE;
+  if (cz < 0 || cz >= D || cy < 0 || cy >= H || cx < 0 || cx >= W) return RINGX_E_SHAPE;
+  int64_t n_in, n_out;
+  if (!mul_ok(C, D, &n_in) || !mul_ok(n_in, H, &n_in) || !mul_ok(n_in, W, &n_in))
+    return RINGX_E_SHAPE;
+  if (D > INT32_MAX / 2 || H > INT32_MAX / 2 || W > INT32_MAX / 2) return RINGX_E_SHAPE;
+  const int64_t gz = sz / k, gy = sy / k, gx = sx / k;
+  if (!mul_ok(C, gz, &n_out) || !mul_ok(n_out, gy, &n_out) || !mul_ok(n_out, gx, &n_out))
+    return RINGX_E_SHAPE;
+  if ((n_out + 255) / 256 > 0xffffffffll) return RINGX_E_SHAPE;
+  if (!aligned16(field) || !aligned16(tokens)) return RINGX_E_ALIGN;
+  if (overlap(span(field, n_in * 4), span(tokens, n_out * esize(out_dtype))))
+    return RINGX_E_ALIAS;
+  ringx::TokArgs a;
+  a.field = field, a.tokens = tokens, a.out_bf16 = out_dtype == RINGX_BF16, a.stream = stream;
+  a.C = C, a.D = D, a.H = H, a.W = W, a.k = k, a.p = p, a.gz = gz, a.gy = gy, a.gx = gx;
+  // first cell of the subdomain, size // 2 cells before the centre, taken periodically
+  a.z0 = ((cz - sz / 2) % D + D) % D;
+  a.y0 = ((cy - sy / 2) % H + H) % H;
+  a.x0 = ((cx - sx / 2) % W + W) % W;
+  double wd[ringx::kMaxTokFilter], total = 0.0;
+  for (int64_t i = 0; i < k; ++i) {
+    const double u = (double)i - (double)(k - 1) / 2.0;
+    wd[i] = std::exp(-u * u / (2.0 * (double)sigma * (double)sigma));
+    total += wd[i];
+  }
+  for (int64_t i = 0; i < k; ++i) a.w.w[i] = (float)(wd[i] / total);
+  return hip_status(ringx::launch_tt_tokenize(a));
+}
+
 }  // extern "C"
+
 

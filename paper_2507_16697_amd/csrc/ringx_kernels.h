@@ -60,6 +60,22 @@ struct BwdArgs {
   hipStream_t stream = nullptr;
 };
 
+// One fidelity mode of the multi-fidelity tokenizer (tt_tokenize.hip).
+constexpr int kMaxTokFilter = 32;
+struct TokWeights {
+  float w[kMaxTokFilter];       // normalised 1D Gaussian weights, w[0 .. k-1]
+};
+struct TokArgs {
+  const float* field = nullptr;  // [C, D, H, W] fp32
+  void* tokens = nullptr;        // [L, C p^3], fp32 or bf16
+  int64_t C = 0, D = 0, H = 0, W = 0, k = 1, p = 1;
+  int64_t gz = 0, gy = 0, gx = 0;   // filtered grid: subdomain size / k
+  int64_t z0 = 0, y0 = 0, x0 = 0;   // first subdomain cell, in [0, D) x [0, H) x [0, W)
+  TokWeights w{};
+  bool out_bf16 = false;
+  hipStream_t stream = nullptr;
+};
+
 hipError_t launch_fwd_bf16(const FwdArgs& a, FwdMode mode);
 hipError_t launch_fwd_f32(const FwdArgs& a, FwdMode mode);
 hipError_t launch_lse_merge(const MergeArgs& a);
@@ -68,6 +84,8 @@ hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a);
 hipError_t launch_bwd_dq_bf16(const BwdArgs& a);
 hipError_t launch_bwd_dkdv_f32(const BwdArgs& a);
 hipError_t launch_bwd_dq_f32(const BwdArgs& a);
+
+hipError_t launch_tt_tokenize(const TokArgs& a);
 
 int64_t fwd_bf16_workgroups(int64_t BH, int64_t Nq, int64_t d);
 

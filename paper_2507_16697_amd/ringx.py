@@ -34,7 +34,7 @@ STATUS_NAMES = {
 EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "ringx_attn_bwd",
             "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv", "ringx_attn_bwd_dq",
             "ringx_attn_fwd_step", "ringx_attn_bwd_step", "ringx_attn_fwd_gqa",
-            "ringx_attn_bwd_gqa", "ringx_bwd_workspace_bytes",
+            "ringx_attn_bwd_gqa", "ringx_tt_tokenize", "ringx_bwd_workspace_bytes",
             "ringx_chunk_bounds", "ringx_status_str")
 
 
@@ -80,6 +80,8 @@ def lib() -> ctypes.CDLL:
         L.ringx_attn_bwd_gqa.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I,
                                          _I, _I, ctypes.c_float, ctypes.c_int, ctypes.c_int, _P,
                                          ctypes.c_size_t, _P]
+        L.ringx_tt_tokenize.argtypes = [_P, _P, _I, _I, _I, _I, _I, _I, _I, _I, _I, _I,
+                                        ctypes.c_float, ctypes.c_int, _P]
         L.ringx_bwd_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, ctypes.c_int]
         L.ringx_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.ringx_chunk_bounds.argtypes = [_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
@@ -88,7 +90,8 @@ def lib() -> ctypes.CDLL:
         for name in ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge",
                      "ringx_attn_bwd", "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv",
                      "ringx_attn_bwd_dq", "ringx_attn_fwd_step", "ringx_attn_bwd_step",
-                     "ringx_attn_fwd_gqa", "ringx_attn_bwd_gqa", "ringx_chunk_bounds"):
+                     "ringx_attn_fwd_gqa", "ringx_attn_bwd_gqa", "ringx_tt_tokenize",
+                     "ringx_chunk_bounds"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -352,3 +355,25 @@ def ringx_attn_bwd_gqa(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=
                                   ws.numel(), _stream(stream))
     _check("ringx_attn_bwd_gqa", st)
     return dq, dk, dv
+
+
+def ringx_tt_tokenize(field, k: int, ratio: int, centre, p: int, sigma=None, out_dtype=None,
+                      tokens=None, stream=None):
+    """One fidelity mode of the multi-fidelity tokenizer: field [C, D, H, W] fp32 on the GPU ->
+    tokens [L, C p^3] (fp32 by default).  sigma defaults to k / 2."""
+    torch = _torch()
+    _dev(field)
+    if field.dtype != torch.float32:
+        raise ValueError("field must be fp32")
+    C, D, H, W = field.shape
+    out_dtype = out_dtype or torch.float32
+    L = (D // (ratio * k * p)) * (H // (ratio * k * p)) * (W // (ratio * k * p))
+    if tokens is None:
+        tokens = torch.empty((L, C * p ** 3), dtype=out_dtype, device=field.device)
+    _dev(tokens)
+    sigma = float(k) / 2.0 if sigma is None else float(sigma)
+    cz, cy, cx = (int(c) for c in centre)
+    st = lib().ringx_tt_tokenize(field.data_ptr(), tokens.data_ptr(), C, D, H, W, k, ratio, cz,
+                                 cy, cx, p, sigma, _dtype_code(tokens), _stream(stream))
+    _check("ringx_tt_tokenize", st)
+    return tokens

@@ -205,3 +205,24 @@ def test_gqa_validation():
                                     wsb, None)
 
     assert bwd_gqa(Hkv=3) == SHAPE and bwd_gqa(ws=0) == WORKSPACE
+
+
+def test_tokenizer_validation():
+    L = ringx.lib()
+    FP, TP = QP, OP
+
+    def tok(C=4, D=64, H=64, W=64, k=4, ratio=2, cz=0, cy=0, cx=0, p=1, sigma=2.0, dt=FP32,
+            field=FP, tokens=TP):
+        return L.ringx_tt_tokenize(field, tokens, C, D, H, W, k, ratio, cz, cy, cx, p, sigma, dt,
+                                   None)
+
+    assert tok(field=0) == NULLPTR and tok(tokens=0) == NULLPTR
+    assert tok(C=0) == SHAPE and tok(k=0) == SHAPE and tok(ratio=0) == SHAPE and tok(p=0) == SHAPE
+    assert tok(ratio=3) == SHAPE                    # 64 % 3
+    assert tok(k=8, p=8) == SHAPE                   # k p does not divide 32
+    assert tok(cz=64) == SHAPE and tok(cx=-1) == SHAPE
+    assert tok(sigma=0.0) == SHAPE and tok(sigma=float("nan")) == SHAPE
+    assert tok(k=33, D=66 * 32, H=66 * 32, W=66 * 32, ratio=1) == UNSUP
+    assert tok(dt=9) == UNSUP
+    assert tok(tokens=TP + 4) == ALIGN
+    assert tok(tokens=FP + 1024) == ALIAS
