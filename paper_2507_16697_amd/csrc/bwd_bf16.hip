@@ -243,6 +243,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     }
     // P and dS (fp32) -> bf16 B operands.  Accumulator r of block b is query
     // 32b + 8(r/4) + 4g + r%4; the 8 queries of k-step 2b+h are accumulators 8h .. 8h+7.
+    // the vector work goes ahead of the other wave's matrix products on the SIMD
+    __builtin_amdgcn_s_setprio(1);
     bf16x8 pf[2 * C::kQB], sf[2 * C::kQB];
 #pragma unroll
     for (int b = 0; b < C::kQB; ++b) {
@@ -283,6 +285,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
         sf[2 * b + h] = __builtin_bit_cast(bf16x8, ws);
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     // dV^T += dO^T P, dK^T += Q^T dS
 #pragma unroll
     for (int ks = 0; ks < 2 * C::kQB; ++ks) {

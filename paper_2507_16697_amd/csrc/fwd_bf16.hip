@@ -253,6 +253,10 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
       issue_tile<D>(kb, lk + P * C::kTileBytes, t2.start, t2.hi, goff, grow, wave);
     if (t1.start < Nk)
       issue_tile<D>(vb, lv + (1 - P) * C::kTileBytes, t1.start, t1.hi, goff, grow, wave);
+    // The vector work of this half (exponentials, row sums) is the longer chain; it issues ahead
+    // of the other wave's matrix products on the SIMD, which fill the gaps (priority drops again
+    // for the P V half).
+    __builtin_amdgcn_s_setprio(1);
 
     // last tile of a chunk: keys past the chunk end (clamped copies of its last key) add nothing.
     // The row max needs no mask: a copy's score equals that of a valid key.
@@ -318,6 +322,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     }
     __builtin_amdgcn_sched_barrier(0);
 
+    __builtin_amdgcn_s_setprio(0);
     // O += V_j^T P_j on the matrix cores; row max of S_{j+1} on the ALU
     const char* vbuf = lds_v + P * C::kTileBytes;
 #pragma unroll

@@ -72,19 +72,21 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t w, uint32_t n) {
 // One 16-byte direct global->LDS load per lane (global_load_lds_dwordx4): the LDS destination is
 // lds_base + 16 * lane.  Issued through inline asm so that the compiler does not serialise later
 // LDS reads of other buffers behind it.  The asm sets m0, which the compiler never uses in these
-// kernels (a build test checks the generated code); callers publish the data with
-// wait_vmem_all() followed by a workgroup barrier.
+// kernels (a build test checks the generated code); an LDS DMA that reads m0 right after a scalar
+// write of it needs one wait state on this chip family, hence the s_nop (the compiler's hazard
+// recognizer does not look inside inline asm).  Callers publish the data with wait_vmem_all()
+// followed by a workgroup barrier.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void load_lds16(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                :
                : "s"(lds_base), "v"(gptr)
                : "memory", "m0");
 }
 // Same with 4 bytes per lane: LDS destination = lds_base + 4 * lane.
 __device__ __forceinline__ void load_lds4(const void* gptr, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off"
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
                :
                : "s"(lds_base), "v"(gptr)
                : "memory", "m0");

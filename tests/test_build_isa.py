@@ -32,7 +32,9 @@ def test_m0_only_feeds_direct_lds_loads(src, tmp_path):
     assert uses, "expected direct LDS loads"
     for i in uses:
         assert re.match(r"s_mov_b32 m0, s\d+$", code[i]), code[i]
-        assert re.match(r"global_load_lds_dword(x4)? ", code[i + 1]), code[i + 1]
+        # one wait state between the scalar write of m0 and the LDS DMA that reads it
+        assert code[i + 1] == "s_nop 0", code[i + 1]
+        assert re.match(r"global_load_lds_dword(x4)? ", code[i + 2]), code[i + 2]
 
 
 @pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "merge.hip", "bwd_pre.hip"])
