@@ -257,6 +257,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
         dqacc[c] = mfma32(__builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7), sf[s], dqacc[c]);
       }
     }
+    // transposed K reads run ahead of the matrix products that consume them
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int i = 0; i < C::kKSteps * C::kCT; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
 
     if (start + C::kBK >= hi) ++r;
     if (!has_next) break;
