@@ -300,9 +300,10 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
         dkt[c] = mfma32(__builtin_shufflevector(q0v, q1v, 0, 1, 2, 3, 4, 5, 6, 7), sf[ks], dkt[c]);
       }
     }
+    // transposed Q / dO reads run ahead of the matrix products that consume them
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-    for (int i = 0; i < 2 * C::kQB * C::kCT; ++i) {
+    for (int i = 0; i < 4 * C::kQB * C::kCT; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
