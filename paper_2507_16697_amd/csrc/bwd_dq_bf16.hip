@@ -153,6 +153,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
   }
   const float nl = -lse[bh * Nq + qi] * kLog2e;
   const float dq_d = delta[bh * Nq + qi];
+  // the dP accumulators start from -D (the same for every key of this lane's query), so that they
+  // come out of the matrix cores as dP - D
+  f32x16 pinit;
+#pragma unroll
+  for (int rr = 0; rr < 16; ++rr) pinit[rr] = -dq_d;
 
   int koff[C::kDSteps];
 #pragma unroll
@@ -205,7 +210,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
 #pragma unroll
     for (int kt = 0; kt < C::kKTiles; ++kt) {
       sacc[kt] = f32x16{};
-      pacc[kt] = f32x16{};
+      pacc[kt] = pinit;
     }
 #pragma unroll
     for (int s = 0; s < C::kDSteps; ++s) {
@@ -240,7 +245,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
           const int r0 = 8 * h + 2 * e;
           const float p0 = fast_exp2(__builtin_fmaf(sacc[kt][r0], c2, nl));
           const float p1 = fast_exp2(__builtin_fmaf(sacc[kt][r0 + 1], c2, nl));
-          w[e] = pack_bf16x2(p0 * (pacc[kt][r0] - dq_d), p1 * (pacc[kt][r0 + 1] - dq_d));
+          w[e] = pack_bf16x2(p0 * pacc[kt][r0], p1 * pacc[kt][r0 + 1]);
         }
         sf[2 * kt + h] = __builtin_bit_cast(bf16x8, w);
       }
