@@ -5,8 +5,10 @@
 //   out     = sum_r w_r part_out[r] / sum_r w_r,   lse = lse_max + log(sum_r w_r)
 //
 // HBM-bound: each output row reads R fp32 rows of d values and R log-sum-exps once.  Vector path:
-// one thread per 4 consecutive columns of a row (16-byte loads, consecutive threads cover a row);
-// scalar path for head dims that are not a multiple of 4 (fp32 output only).
+// one thread per 4 consecutive columns of a row (16-byte loads, consecutive threads cover a row),
+// the partial loop unrolled so that several rows are in flight per thread, and the partials and
+// the output streamed with non-temporal loads and stores (each is touched once); scalar path for
+// head dims that are not a multiple of 4 (fp32 output only).
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
@@ -27,12 +29,16 @@ __global__ __launch_bounds__(kMergeThreads) void merge_vec4_kernel(
   const int c = (int)(idx % quads) * 4;
 
   float M = -INFINITY;
+#pragma unroll 8
   for (int r = 0; r < R; ++r) M = fmaxf(M, part_lse[(int64_t)r * rows + row]);
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   float den = 0.f;
+  // unrolled so that several partial rows are in flight per thread
+#pragma unroll 8
   for (int r = 0; r < R; ++r) {
     const float w = fast_exp2((part_lse[(int64_t)r * rows + row] - M) * kLog2e);
-    const f32x4 x = *reinterpret_cast<const f32x4*>(part_out + ((int64_t)r * rows + row) * d + c);
+    const f32x4 x = __builtin_nontemporal_load(
+        reinterpret_cast<const f32x4*>(part_out + ((int64_t)r * rows + row) * d + c));
     acc += x * w;
     den += w;
   }
@@ -42,9 +48,11 @@ __global__ __launch_bounds__(kMergeThreads) void merge_vec4_kernel(
     u32x2 w2;
     w2[0] = pack_bf16x2(acc[0], acc[1]);
     w2[1] = pack_bf16x2(acc[2], acc[3]);
-    *reinterpret_cast<u32x2*>(reinterpret_cast<__bf16*>(out) + row * d + c) = w2;
+    __builtin_nontemporal_store(
+        w2, reinterpret_cast<u32x2*>(reinterpret_cast<__bf16*>(out) + row * d + c));
   } else {
-    *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(out) + row * d + c) = acc;
+    __builtin_nontemporal_store(
+        acc, reinterpret_cast<f32x4*>(reinterpret_cast<float*>(out) + row * d + c));
   }
   if (c == 0) lse[row] = M + logf(den);
 }

@@ -107,7 +107,10 @@ __global__ __launch_bounds__(kTokThreads) void tt_tokenize_rows_kernel(
       const float wij = w.w[i] * w.w[j];
       const float* rowp = fc + ((int64_t)z * H + y) * W;
       if (contiguous) {
-        const f32x4 v = *reinterpret_cast<const f32x4*>(rowp + xs);
+        // the field is streamed once: non-temporal loads, except for the unfiltered crop (k = 1),
+        // whose short row segments are latency-bound
+        const f32x4* vp = reinterpret_cast<const f32x4*>(rowp + xs);
+        const f32x4 v = K > 1 ? __builtin_nontemporal_load(vp) : *vp;
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wij, v[e], acc[e]);
       } else if (active) {
