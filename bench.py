@@ -218,14 +218,16 @@ def main():
                             "tflops": tf(2 * U, fwd_ms),
                             "traffic": load_traffic("fwd_bf16", w.name,
                                                     kernel_source_hash(["fwd_bf16.hip", "ringx_device.h"]))},
-        "bwd_dkdv_kernel": {"ms": dkdv_ms, "flops": 2 * U,
-                            "work": "4*B*H*Nq*Nk*d credited (dV, dK); S and dP recomputed",
-                            "tflops": tf(2 * U, dkdv_ms),
+        # the backward's four algorithmic contractions (dV, dP, dK, dQ) are credited to the kernel
+        # that computes them first: dP is part of the dK/dV pass, the dQ pass recomputes S and dP
+        "bwd_dkdv_kernel": {"ms": dkdv_ms, "flops": 3 * U,
+                            "work": "6*B*H*Nq*Nk*d credited (dV, dP, dK); S recomputed",
+                            "tflops": tf(3 * U, dkdv_ms),
                             "traffic": load_traffic("bwd_dkdv", w.name,
                                                     kernel_source_hash(["bwd_bf16.hip", "ringx_device.h"]))},
-        "bwd_dq_kernel": {"ms": dq_ms, "flops": 2 * U,
-                          "work": "4*B*H*Nq*Nk*d credited (dP, dQ); S recomputed",
-                          "tflops": tf(2 * U, dq_ms),
+        "bwd_dq_kernel": {"ms": dq_ms, "flops": U,
+                          "work": "2*B*H*Nq*Nk*d credited (dQ); S and dP recomputed",
+                          "tflops": tf(U, dq_ms),
                           "traffic": load_traffic("bwd_dq", w.name,
                                                   kernel_source_hash(["bwd_dq_bf16.hip", "ringx_device.h"]))},
         "bwd_pre_bf16_kernel": {"ms": pre_ms, "bytes": B * H * Nq * (4 * d + 4),
