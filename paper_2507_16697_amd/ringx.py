@@ -142,6 +142,40 @@ def _dev(*ts):
             raise ValueError("tensors must be contiguous [B, H, N, d]")
 
 
+def _expect(name, t, shape, dtype, device):
+    """The kernels size every buffer from q and k: a tensor of another shape, dtype or device
+    would be read or written out of bounds, so it is refused here."""
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if t.device != device:
+        raise ValueError(f"{name}: on {t.device}, expected {device}")
+
+
+def _qkv(q, k, v, heads_kv=None):
+    """Shapes of q [B,H,Nq,d] and k, v [B,Hkv,Nk,d] (Hkv = H unless heads_kv is allowed to
+    differ); returns (B, H, Hkv, Nq, Nk, d)."""
+    if q.dim() != 4 or k.dim() != 4:
+        raise ValueError("q, k and v must be 4-D [B, H, N, d]")
+    _dtype_code(q)
+    B, H, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
+    if heads_kv is None and Hkv != H:
+        raise ValueError(f"k has {Hkv} heads, q has {H}")
+    _expect("k", k, (B, Hkv, Nk, d), q.dtype, q.device)
+    _expect("v", v, (B, Hkv, Nk, d), q.dtype, q.device)
+    return B, H, Hkv, Nq, Nk, d
+
+
+def _check_grad_inputs(q, dout, lse, delta):
+    torch = _torch()
+    B, H, Nq, _ = q.shape
+    _expect("dout", dout, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
+    _expect("delta", delta, (B, H, Nq), torch.float32, q.device)
+
+
 def _stream(stream):
     torch = _torch()
     if stream is None:
@@ -159,13 +193,14 @@ def ringx_attn_fwd(q, k, v, R: int, scale=None, out=None, lse=None, stream=None)
     """Merged ring-chunked forward.  Returns (out [B,H,Nq,d] in q's dtype, lse [B,H,Nq] fp32)."""
     torch = _torch()
     _dev(q, k, v)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
     _dev(out, lse)
+    _expect("out", out, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
     st = lib().ringx_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                               lse.data_ptr(), B, H, Nq, Nk, d, R, _scale(scale, d),
                               _dtype_code(q), _stream(stream))
@@ -178,13 +213,14 @@ def ringx_attn_fwd_partials(q, k, v, R: int, scale=None, part_out=None, part_lse
     """Per-chunk local results: (part_out [R,B,H,Nq,d] fp32, part_lse [R,B,H,Nq] fp32)."""
     torch = _torch()
     _dev(q, k, v)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
     if part_out is None:
         part_out = torch.empty((R, B, H, Nq, d), dtype=torch.float32, device=q.device)
     if part_lse is None:
         part_lse = torch.empty((R, B, H, Nq), dtype=torch.float32, device=q.device)
     _dev(part_out, part_lse)
+    _expect("part_out", part_out, (R, B, H, Nq, d), torch.float32, q.device)
+    _expect("part_lse", part_lse, (R, B, H, Nq), torch.float32, q.device)
     st = lib().ringx_attn_fwd_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                        part_out.data_ptr(), part_lse.data_ptr(), B, H, Nq, Nk, d,
                                        R, _scale(scale, d), _dtype_code(q), _stream(stream))
@@ -196,12 +232,20 @@ def ringx_lse_merge(part_out, part_lse, out_dtype=None, out=None, lse=None, stre
     """Eq. (5) merge of R partials.  Returns (out [B,H,Nq,d] in out_dtype, lse [B,H,Nq] fp32)."""
     torch = _torch()
     _dev(part_out, part_lse)
+    if part_out.dim() != 5:
+        raise ValueError("part_out must be 5-D [R, B, H, Nq, d]")
     R, B, H, Nq, d = part_out.shape
+    dev = part_out.device
+    _expect("part_out", part_out, (R, B, H, Nq, d), torch.float32, dev)
+    _expect("part_lse", part_lse, (R, B, H, Nq), torch.float32, dev)
     if out is None:
-        out = torch.empty((B, H, Nq, d), dtype=out_dtype or torch.float32, device=part_out.device)
+        out = torch.empty((B, H, Nq, d), dtype=out_dtype or torch.float32, device=dev)
     if lse is None:
-        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=part_out.device)
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=dev)
     _dev(out, lse)
+    _dtype_code(out)
+    _expect("out", out, (B, H, Nq, d), out.dtype, dev)
+    _expect("lse", lse, (B, H, Nq), torch.float32, dev)
     st = lib().ringx_lse_merge(part_out.data_ptr(), part_lse.data_ptr(), out.data_ptr(),
                                lse.data_ptr(), R, B, H, Nq, d, _dtype_code(out), _stream(stream))
     _check("ringx_lse_merge", st)
@@ -213,8 +257,10 @@ def ringx_attn_bwd(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None
     """Recompute backward.  Returns fp32 (dq, dk, dv); dk/dv are added to when accumulate_dkv."""
     torch = _torch()
     _dev(q, k, v, out, dout, lse)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
+    _expect("out", out, q.shape, q.dtype, q.device)
+    _expect("dout", dout, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
     f32 = dict(dtype=torch.float32, device=q.device)
     if dq is None:
         dq = torch.empty((B, H, Nq, d), **f32)
@@ -227,6 +273,11 @@ def ringx_attn_bwd(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
     _dev(dq, dk, dv, workspace)
+    _expect("dq", dq, (B, H, Nq, d), torch.float32, q.device)
+    _expect("dk", dk, (B, H, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, H, Nk, d), torch.float32, q.device)
+    if workspace.device != q.device:
+        raise ValueError(f"workspace: on {workspace.device}, expected {q.device}")
     st = lib().ringx_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                               dout.data_ptr(), lse.data_ptr(), dq.data_ptr(), dk.data_ptr(),
                               dv.data_ptr(), B, H, Nq, Nk, d, R, _scale(scale, d), code,
@@ -240,10 +291,15 @@ def ringx_bwd_preprocess(out, dout, delta=None, stream=None):
     """delta [B,H,Nq] fp32 = rowsum(dout * out)."""
     torch = _torch()
     _dev(out, dout)
+    if out.dim() != 4:
+        raise ValueError("out must be 4-D [B, H, Nq, d]")
+    _dtype_code(out)
     B, H, Nq, d = out.shape
+    _expect("dout", dout, out.shape, out.dtype, out.device)
     if delta is None:
         delta = torch.empty((B, H, Nq), dtype=torch.float32, device=out.device)
     _dev(delta)
+    _expect("delta", delta, (B, H, Nq), torch.float32, out.device)
     st = lib().ringx_bwd_preprocess(out.data_ptr(), dout.data_ptr(), delta.data_ptr(), B, H, Nq,
                                     d, _dtype_code(out), _stream(stream))
     _check("ringx_bwd_preprocess", st)
@@ -255,14 +311,16 @@ def ringx_attn_bwd_dkdv(q, k, v, dout, lse, delta, R: int, scale=None, dk=None, 
     """Key/value gradients of every chunk.  Returns fp32 (dk, dv)."""
     torch = _torch()
     _dev(q, k, v, dout, lse, delta)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
+    _check_grad_inputs(q, dout, lse, delta)
     f32 = dict(dtype=torch.float32, device=q.device)
     if dk is None:
         dk = torch.zeros((B, H, Nk, d), **f32)
     if dv is None:
         dv = torch.zeros((B, H, Nk, d), **f32)
     _dev(dk, dv)
+    _expect("dk", dk, (B, H, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, H, Nk, d), torch.float32, q.device)
     st = lib().ringx_attn_bwd_dkdv(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
                                    lse.data_ptr(), delta.data_ptr(), dk.data_ptr(), dv.data_ptr(),
                                    B, H, Nq, Nk, d, R, _scale(scale, d), _dtype_code(q),
@@ -275,11 +333,12 @@ def ringx_attn_bwd_dq(q, k, v, dout, lse, delta, R: int, scale=None, dq=None, st
     """Query gradient accumulated over every chunk.  Returns fp32 dq."""
     torch = _torch()
     _dev(q, k, v, dout, lse, delta)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
+    _check_grad_inputs(q, dout, lse, delta)
     if dq is None:
         dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
     _dev(dq)
+    _expect("dq", dq, (B, H, Nq, d), torch.float32, q.device)
     st = lib().ringx_attn_bwd_dq(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
                                  lse.data_ptr(), delta.data_ptr(), dq.data_ptr(), B, H, Nq, Nk, d,
                                  R, _scale(scale, d), _dtype_code(q), _stream(stream))
@@ -290,9 +349,11 @@ def ringx_attn_bwd_dq(q, k, v, dout, lse, delta, R: int, scale=None, dq=None, st
 def ringx_attn_fwd_step(q, k, v, out_acc, lse_acc, first: bool, scale=None, stream=None):
     """One ring step: merge q's attention over the chunk k, v into the running fp32
     (out_acc [B,H,Nq,d], lse_acc [B,H,Nq]) in place (Eq. (5)); first=True starts it."""
+    torch = _torch()
     _dev(q, k, v, out_acc, lse_acc)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
+    _expect("out_acc", out_acc, (B, H, Nq, d), torch.float32, q.device)
+    _expect("lse_acc", lse_acc, (B, H, Nq), torch.float32, q.device)
     st = lib().ringx_attn_fwd_step(q.data_ptr(), k.data_ptr(), v.data_ptr(), out_acc.data_ptr(),
                                    lse_acc.data_ptr(), B, H, Nq, Nk, d, _scale(scale, d),
                                    _dtype_code(q), 1 if first else 0, _stream(stream))
@@ -304,9 +365,13 @@ def ringx_attn_bwd_step(q, k, v, dout, lse, delta, dq_acc, dk, dv, accumulate_dq
                         accumulate_dkv: bool = False, scale=None, stream=None):
     """One ring step of the backward for the chunk k, v: its dk, dv (fp32, written or added to)
     and its contribution to dq_acc (added to, or written when accumulate_dq is False)."""
+    torch = _torch()
     _dev(q, k, v, dout, lse, delta, dq_acc, dk, dv)
-    B, H, Nq, d = q.shape
-    Nk = k.shape[2]
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
+    _check_grad_inputs(q, dout, lse, delta)
+    _expect("dq_acc", dq_acc, (B, H, Nq, d), torch.float32, q.device)
+    _expect("dk", dk, (B, H, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, H, Nk, d), torch.float32, q.device)
     st = lib().ringx_attn_bwd_step(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
                                    lse.data_ptr(), delta.data_ptr(), dq_acc.data_ptr(),
                                    dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nk, d, _scale(scale, d),
@@ -320,13 +385,14 @@ def ringx_attn_fwd_gqa(q, k, v, R: int, scale=None, out=None, lse=None, stream=N
     """Grouped-query attention: q [B,H,Nq,d], k, v [B,Hkv,Nk,d] with Hkv dividing H."""
     torch = _torch()
     _dev(q, k, v)
-    B, H, Nq, d = q.shape
-    Hkv, Nk = k.shape[1], k.shape[2]
+    B, H, Hkv, Nq, Nk, d = _qkv(q, k, v, heads_kv=True)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
     _dev(out, lse)
+    _expect("out", out, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
     st = lib().ringx_attn_fwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                   lse.data_ptr(), B, H, Hkv, Nq, Nk, d, R, _scale(scale, d),
                                   _dtype_code(q), _stream(stream))
@@ -339,13 +405,18 @@ def ringx_attn_bwd_gqa(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=
     """Backward of ringx_attn_fwd_gqa: fp32 dq [B,H,Nq,d], dk, dv [B,Hkv,Nk,d] (group sums)."""
     torch = _torch()
     _dev(q, k, v, out, dout, lse)
-    B, H, Nq, d = q.shape
-    Hkv, Nk = k.shape[1], k.shape[2]
+    B, H, Hkv, Nq, Nk, d = _qkv(q, k, v, heads_kv=True)
+    _expect("out", out, q.shape, q.dtype, q.device)
+    _expect("dout", dout, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
     f32 = dict(dtype=torch.float32, device=q.device)
     dq = torch.empty((B, H, Nq, d), **f32) if dq is None else dq
     dk = torch.zeros((B, Hkv, Nk, d), **f32) if dk is None else dk
     dv = torch.zeros((B, Hkv, Nk, d), **f32) if dv is None else dv
     _dev(dq, dk, dv)
+    _expect("dq", dq, (B, H, Nq, d), torch.float32, q.device)
+    _expect("dk", dk, (B, Hkv, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, Hkv, Nk, d), torch.float32, q.device)
     nbytes = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, _dtype_code(q))
     ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
     st = lib().ringx_attn_bwd_gqa(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
@@ -371,6 +442,8 @@ def ringx_tt_tokenize(field, k: int, ratio: int, centre, p: int, sigma=None, out
     if tokens is None:
         tokens = torch.empty((L, C * p ** 3), dtype=out_dtype, device=field.device)
     _dev(tokens)
+    _dtype_code(tokens)
+    _expect("tokens", tokens, (L, C * p ** 3), tokens.dtype, field.device)
     sigma = float(k) / 2.0 if sigma is None else float(sigma)
     cz, cy, cx = (int(c) for c in centre)
     st = lib().ringx_tt_tokenize(field.data_ptr(), tokens.data_ptr(), C, D, H, W, k, ratio, cz,

@@ -336,3 +336,42 @@ def test_errors_leave_outputs_untouched():
         ringx.ringx_attn_fwd(q, k, k.clone(), 1, scale=float("nan"), out=out, lse=lse)
     torch.cuda.synchronize()
     assert torch.all(out == 7.0) and torch.all(lse == 3.0)
+
+
+def test_mismatched_buffers_are_refused_before_launch():
+    """Every wrapper checks each tensor against the sizes the kernels derive from q and k; a
+    mismatch raises on the host and nothing is launched (the outputs keep their contents)."""
+    dev = "cuda"
+    bf = dict(dtype=torch.bfloat16, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    q = torch.randn((1, 2, 16, 64), **bf)
+    k = torch.randn((1, 2, 40, 64), **bf)
+    v = torch.randn((1, 2, 40, 64), **bf)
+    out = torch.full((1, 2, 16, 64), 7.0, **bf)
+    lse = torch.full((1, 2, 16), 3.0, **f32)
+    with pytest.raises(ValueError, match="v: shape"):
+        ringx.ringx_attn_fwd(q, k, v[:, :, :39].contiguous(), 2, out=out, lse=lse)
+    with pytest.raises(ValueError, match="lse: shape"):
+        ringx.ringx_attn_fwd(q, k, v, 2, out=out, lse=torch.zeros((1, 2, 15), **f32))
+    with pytest.raises(TypeError, match="out: dtype"):
+        ringx.ringx_attn_fwd(q, k, v, 2, out=torch.zeros((1, 2, 16, 64), **f32), lse=lse)
+    do = torch.randn_like(q)
+    with pytest.raises(TypeError, match="dk: dtype"):
+        ringx.ringx_attn_bwd(q, k, v, out, do, lse, 2, dk=torch.zeros((1, 2, 40, 64), **bf))
+    with pytest.raises(ValueError, match="dv: shape"):
+        ringx.ringx_attn_bwd(q, k, v, out, do, lse, 2, dv=torch.zeros((1, 2, 39, 64), **f32))
+    delta = torch.zeros((1, 2, 16), **f32)
+    with pytest.raises(ValueError, match="delta: shape"):
+        ringx.ringx_attn_bwd_dq(q, k, v, do, lse, delta[:, :, :8].contiguous(), 2)
+    with pytest.raises(TypeError, match="out_acc: dtype"):
+        ringx.ringx_attn_fwd_step(q, k, v, torch.zeros((1, 2, 16, 64), **bf), lse, True)
+    with pytest.raises(ValueError, match="dk: shape"):
+        ringx.ringx_attn_bwd_gqa(q, k[:, :1].contiguous(), v[:, :1].contiguous(), out, do, lse, 2,
+                                 dk=torch.zeros((1, 2, 40, 64), **f32))
+    with pytest.raises(ValueError, match="part_lse: shape"):
+        ringx.ringx_lse_merge(torch.zeros((2, 1, 2, 16, 64), **f32), torch.zeros((2, 1, 2, 8), **f32))
+    field = torch.zeros((2, 8, 8, 8), **f32)
+    with pytest.raises(ValueError, match="tokens: shape"):
+        ringx.ringx_tt_tokenize(field, 2, 1, (4, 4, 4), 1, tokens=torch.zeros((63, 2), **f32))
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0) and torch.all(lse == 3.0)
