@@ -4,8 +4,12 @@
 // every chunk r the thread runs an online softmax over the chunk's keys (Eqs. (2)-(4) of arXiv
 // 2507.16697 Sec. III-A), forms the chunk's local result (loc_out_r, loc_lse_r), and either writes
 // it (partials mode) or folds it into the Eq. (5) merge.  The merged output accumulates in place in
-// the fp32 output row, which only this thread touches.  Step mode (R = 1) folds the one chunk into
-// a running fp32 (acc_out, acc_lse) left by earlier ring steps.
+// the fp32 output row, which only this thread touches: unnormalised, with Eq. (5)'s terms
+// exp(loc_lse_r - M) loc_out_r = exp(m_r - M) o_r and exp(loc_lse_r - M) = exp(m_r - M) l_r kept
+// relative to a running reference M (the largest m_r so far), and one division and one log at
+// the end, so that rounding does not build up over many chunks.  Step mode (R = 1) folds the one
+// chunk into a running fp32 (acc_out, acc_lse) left by earlier ring steps, which by the step
+// contract holds the normalised result.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
@@ -40,6 +44,8 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
   float* orow = (STEP ? acc_out : out) + (bh * Nq + (active ? qi : 0)) * d;
   // step mode starts from the running result of the earlier ring steps
   float lse_m = (STEP && !first && active) ? acc_lse[bh * Nq + qi] : -INFINITY;
+  // fused mode: reference and denominator of the unnormalised merge
+  float mref = -INFINITY, den = 0.f;
 
   for (int r = 0; r < R; ++r) {
     const int64_t lo = (int64_t)r * Nk / R;
@@ -72,9 +78,27 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
         m = mn;
       }
     }
+    if (!active) continue;
+    if constexpr (!PARTIALS && !STEP) {
+      // Eq. (5) with a running reference: the row holds sum_r exp(m_r - mref) o_r
+      if (m > mref) {
+        const float f = expf(mref - m);   // 0 for the first chunk
+#pragma unroll
+        for (int c = 0; c < DMAX; ++c)
+          if (c < d) orow[c] = (r == 0 ? 0.f : orow[c] * f) + o[c];
+        den = den * f + l;
+        mref = m;
+      } else {
+        const float w = expf(m - mref);
+#pragma unroll
+        for (int c = 0; c < DMAX; ++c)
+          if (c < d) orow[c] = __builtin_fmaf(w, o[c], orow[c]);
+        den = __builtin_fmaf(w, l, den);
+      }
+      continue;
+    }
     const float inv = 1.0f / l;
     const float lse_r = m + logf(l);
-    if (!active) continue;
     if constexpr (PARTIALS) {
       float* po = part_out + (((int64_t)r * BH + bh) * Nq + qi) * d;
 #pragma unroll
@@ -86,17 +110,25 @@ __global__ __launch_bounds__(kF32Threads) void fwd_f32_kernel(
       const float M = fmaxf(lse_m, lse_r);
       const float a = expf(lse_m - M);
       const float b = expf(lse_r - M);
-      const float den = a + b;
-      const float wa = a / den;
-      const float wb = b * inv / den;
+      const float ab = a + b;
+      const float wa = a / ab;
+      const float wb = b * inv / ab;
 #pragma unroll
       for (int c = 0; c < DMAX; ++c)
         if (c < d) orow[c] = (lse_m == -INFINITY ? 0.f : orow[c] * wa) + o[c] * wb;
-      lse_m = M + logf(den);
+      lse_m = M + logf(ab);
     }
   }
-  if constexpr (!PARTIALS) {
-    if (active) (STEP ? acc_lse : lse)[bh * Nq + qi] = lse_m;
+  if constexpr (STEP) {
+    if (active) acc_lse[bh * Nq + qi] = lse_m;
+  } else if constexpr (!PARTIALS) {
+    if (active) {
+      const float inv = 1.0f / den;
+#pragma unroll
+      for (int c = 0; c < DMAX; ++c)
+        if (c < d) orow[c] *= inv;
+      lse[bh * Nq + qi] = mref + logf(den);
+    }
   }
 }
 
