@@ -71,8 +71,8 @@ def test_sweep(case):
         acc_l = torch.empty((B, H, nq), dtype=torch.float32, device="cuda")
         for r in range(R):
             lo, hi = oa.chunk_bounds(nk, R, r)
-            kc = g["k"][:, :, lo:hi].contiguous()
-            vc = g["v"][:, :, lo:hi].contiguous()
+            kc = g["k"][:, :, lo:hi].clone()
+            vc = g["v"][:, :, lo:hi].clone()
             ringx.ringx_attn_fwd_step(g["q"], kc, vc, acc_o, acc_l, r == 0, scale=scale)
         steps = (acc_o, acc_l)
     torch.cuda.synchronize()
@@ -103,3 +103,134 @@ def test_sweep(case):
     print(case, " ".join(f"{k}={e:.2e}" for k, (e, _) in errs.items()), flush=True)
     for key, (e, tol) in errs.items():
         assert e <= tol, (case, key, e)
+
+
+def _inputs(case):
+    i, store, B, hkv, grp, nq, nk, d, R = case
+    H = hkv * grp
+    std, do_std = ((0.5, 1.0) if d == 64 else (2 ** -0.5, 2 ** -0.5)) if store == "bf16" \
+        else (1.0, 1.0)
+    qd = inputs.make_iid(B, H, nq, 1, d, seed=1000 + i, std=std, store=store, with_do=True,
+                         do_std=do_std)
+    kv = inputs.make_iid(B, hkv, 1, nk, d, seed=2000 + i, std=std, store=store, with_do=False)
+    t = {"q": qd["q"], "do": qd["do"], "k": kv["k"], "v": kv["v"]}
+    x = {key: inputs.to_f64(val, store) for key, val in t.items()}
+    g = {key: to_device(val, store) for key, val in t.items()}
+    return x, g, float(np.float32(1 / math.sqrt(d)))
+
+
+def _err(store, key, got, ref, grad=False):
+    if store == "fp32":
+        e = max_abs_err(got, ref)
+        return e / max(1.0, float(np.max(np.abs(ref)))) if grad else e, TOL_F32
+    if key.endswith("lse"):
+        return max_abs_err(got, ref), TOL_BF16_LSE
+    return _bf16_err(got, ref), TOL_BF16_REL_RMS
+
+
+_MHA = [c for c in _cases() if c[4] == 1]
+
+
+@pytest.mark.parametrize("case", _MHA[::2], ids=lambda c: "-".join(str(x) for x in c))
+def test_sweep_partials_and_merge(case):
+    """Every chunk's (loc_out_r, loc_lse_r) against the oracle's, and the standalone Eq. (5)
+    merge of the kernel's partials into bf16 and fp32 outputs."""
+    i, store, B, hkv, grp, nq, nk, d, R = case
+    x, g, scale = _inputs(case)
+    po, pl = ringx.ringx_attn_fwd_partials(g["q"], g["k"], g["v"], R, scale=scale)
+    mo32, ml32 = ringx.ringx_lse_merge(po, pl, out_dtype=torch.float32)
+    # a bf16 merged output needs d % 4 == 0 (the library refuses other head dims for it)
+    mo16 = None
+    if d % 4 == 0:
+        mo16, ml16 = ringx.ringx_lse_merge(po, pl, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    rpo, rpl = oracle.attention_partials(x["q"], x["k"], x["v"], scale, R)
+    ro, rl = oa.lse_merge(rpo, rpl)
+    errs = {"part_out": _err(store, "part_out", to_host_f64(po), rpo),
+            "part_lse": _err(store, "part_lse", to_host_f64(pl), rpl),
+            "merged_out": _err(store, "merged_out", to_host_f64(mo32), ro),
+            "merged_lse": _err(store, "merged_lse", to_host_f64(ml32), rl)}
+    if mo16 is not None:
+        assert torch.equal(ml16, ml32)
+        got16 = to_host_f64(mo16)
+        if store == "bf16":
+            errs["merged_out_bf16"] = (_bf16_err(got16, ro), TOL_BF16_REL_RMS)
+        else:
+            # fp32 partials: only the final rounding to bf16 (at most 2^-8 relative) remains
+            excess = np.abs(got16 - ro) - 2.0 ** -8 * np.abs(ro)
+            errs["merged_out_bf16"] = (float(np.max(excess)), TOL_F32)
+    else:
+        with pytest.raises(ringx.RingxError):
+            ringx.ringx_lse_merge(po, pl, out_dtype=torch.bfloat16)
+    print(case, " ".join(f"{k}={e:.2e}" for k, (e, _) in errs.items()), flush=True)
+    for key, (e, tol) in errs.items():
+        assert e <= tol, (case, key, e)
+
+
+@pytest.mark.parametrize("case", _MHA[1::2], ids=lambda c: "-".join(str(x) for x in c))
+def test_sweep_ring_backward(case):
+    """The backward as R ring steps: each chunk's dK/dV written by its own step, dQ accumulated
+    over the steps, against the oracle's full gradients."""
+    i, store, B, hkv, grp, nq, nk, d, R = case
+    x, g, scale = _inputs(case)
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    delta = ringx.ringx_bwd_preprocess(out, g["do"])
+    dq = torch.empty((B, hkv, nq, d), dtype=torch.float32, device="cuda")
+    dk = torch.empty((B, hkv, nk, d), dtype=torch.float32, device="cuda")
+    dv = torch.empty_like(dk)
+    for r in range(R):
+        lo, hi = oa.chunk_bounds(nk, R, r)
+        dkr = torch.empty((B, hkv, hi - lo, d), dtype=torch.float32, device="cuda")
+        dvr = torch.empty_like(dkr)
+        # chunks in buffers of their own (the library wants 16-byte aligned tensors; a slice of
+        # a row-major tensor starts wherever its first row does)
+        ringx.ringx_attn_bwd_step(g["q"], g["k"][:, :, lo:hi].clone(), g["v"][:, :, lo:hi].clone(),
+                                  g["do"], lse, delta, dq, dkr, dvr, accumulate_dq=r > 0,
+                                  scale=scale)
+        dk[:, :, lo:hi] = dkr
+        dv[:, :, lo:hi] = dvr
+    torch.cuda.synchronize()
+    ro, rl = oracle.attention(x["q"], x["k"], x["v"], scale)
+    rq, rk, rv = oracle.attention_bwd(x["q"], x["k"], x["v"], ro, x["do"], rl, scale)
+    errs = {"dq": _err(store, "dq", to_host_f64(dq), rq, grad=True),
+            "dk": _err(store, "dk", to_host_f64(dk), rk, grad=True),
+            "dv": _err(store, "dv", to_host_f64(dv), rv, grad=True)}
+    print(case, " ".join(f"{k}={e:.2e}" for k, (e, _) in errs.items()), flush=True)
+    for key, (e, tol) in errs.items():
+        assert e <= tol, (case, key, e)
+
+
+def _tok_cases():
+    rng = np.random.default_rng(71)
+    out = []
+    while len(out) < 24:
+        C = int(rng.integers(1, 5))
+        k = int(rng.choice([1, 2, 3, 4, 5, 8, 16]))
+        p = int(rng.choice([1, 2, 3]))
+        ratio = int(rng.choice([1, 2, 3, 4]))
+        n = [int(rng.integers(1, 5)) for _ in range(3)]
+        D, H, W = (ratio * k * p * m for m in n)
+        if C * D * H * W > 4_000_000:
+            continue
+        centre = tuple(int(rng.integers(0, s)) for s in (D, H, W))
+        sigma = float(np.float32(rng.uniform(0.3, 2.0) * k))
+        bf16 = bool(rng.integers(0, 2))
+        out.append((len(out), C, D, H, W, k, ratio, p, centre, sigma, bf16))
+    return out
+
+
+@pytest.mark.parametrize("case", _tok_cases(), ids=lambda c: "-".join(str(x) for x in c[:8]))
+def test_sweep_tokenizer(case):
+    """Fidelity modes of random fields: any filter size (the row kernel for powers of two with
+    4-cell rows, the generic kernel otherwise), ratio, patch, centre (wrapping) and sigma."""
+    j, C, D, H, W, k, ratio, p, centre, sigma, bf16 = case
+    f = np.random.default_rng(300 + j).standard_normal((C, D, H, W)).astype(np.float32)
+    tok = ringx.ringx_tt_tokenize(torch.from_numpy(f).cuda(), k, ratio, centre, p, sigma=sigma,
+                                  out_dtype=torch.bfloat16 if bf16 else torch.float32)
+    torch.cuda.synchronize()
+    ref = oracle.tt_tokenize(f.astype(np.float64), k, ratio, centre, p, sigma)
+    assert tok.shape == ref.shape
+    got = tok.float().cpu().numpy().astype(np.float64)
+    e = _bf16_err(got, ref) if bf16 else max_abs_err(got, ref)
+    print(case, f"err={e:.2e}", flush=True)
+    assert e <= (TOL_BF16_REL_RMS if bf16 else TOL_F32), (case, e)
