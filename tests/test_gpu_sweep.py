@@ -100,6 +100,13 @@ def test_sweep(case):
             errs[key] = (max_abs_err(got[key], ref[key]), TOL_BF16_LSE)
         else:
             errs[key] = (_bf16_err(got[key], ref[key]), TOL_BF16_REL_RMS)
+    if store == "bf16":
+        # every element also within 1.5x the bound of the path's roundings
+        b_out, b_dq, b_dk, b_dv = _rounding_bounds(x, kr, vr, ro, rl, scale)
+        gsum = lambda a: a.reshape(B, hkv, grp, nk, d).sum(axis=2)
+        for key, b in (("out", b_out), ("dq", b_dq), ("dk", gsum(b_dk)), ("dv", gsum(b_dv))):
+            lim = 1.5 * b + 1e-5 * max(1.0, float(np.max(np.abs(ref[key]))))
+            errs[key + "/bound"] = (float(np.max(np.abs(got[key] - ref[key]) / lim)), 1.0)
     print(case, " ".join(f"{k}={e:.2e}" for k, (e, _) in errs.items()), flush=True)
     for key, (e, tol) in errs.items():
         assert e <= tol, (case, key, e)
