@@ -1,54 +1,88 @@
-// Recompute backward of ring-chunked attention, dK/dV part: bf16 MFMA with fp32 accumulation
-// (gfx950).
+// Recompute backward of ring-chunked attention, dK/dV part at head size 128: bf16 MFMA with fp32
+// accumulation (gfx950).  Head size 64 runs the two-waves-per-SIMD kernel in bwd_bf16_d64.hip.
 //
-// One workgroup = 8 waves = one (b, h) and a tile of 128 keys inside one chunk (a key tile never
-// straddles a chunk boundary).  With the merged log-sum-exp saved by the forward, every chunk's
-// gradients are independent (arXiv 2507.16697 Sec. III-A: K/V chunk gradients computed per
-// chunk), so the workgroup sweeps every query tile of BQ queries once -- of every query head that
-// shares the K/V head when G > 1 query heads share one (grouped-query attention).  Wave w owns keys
-// 32*(w%4) .. +31 of the tile and query half w/4 of every query tile, and keeps fp32 dK^T, dV^T
-// accumulators for its keys in registers.  Per query tile:
-//   S   = Q K^T        A = Q rows (LDS),  B = K rows (LDS)              -> lane = key
-//   dP  = dO V^T       A = dO rows (LDS), B = V rows (LDS)
-//   P   = exp2(S*scale*log2e - lse_i*log2e),  dS = P (dP - D_i)        (fp32)
-//   dV^T += dO^T P     A = dO^T by transposed LDS reads, B = P from registers
-//   dK^T += Q^T dS     A = Q^T by transposed LDS reads,  B = dS from registers
-// Q, dO, lse and D of the next query tile arrive by direct global->LDS loads while the current
-// one is processed (double buffered, one barrier per tile).  K and V tiles are row-major in LDS
-// with XOR-swizzled 16-byte chunks.  The two waves sharing a key block add their dK/dV through
-// LDS at the end.  dQ is computed by the query-stationary kernel in bwd_dq_bf16.hip.
+// One workgroup = 4 waves (one per SIMD) = one K/V head and a tile of 128 keys inside one chunk
+// (a key tile never straddles a chunk boundary).  With the merged log-sum-exp saved by the
+// forward, every chunk's gradients are independent (arXiv 2507.16697 Sec. III-A: K/V chunk
+// gradients computed per chunk), so the workgroup sweeps every query of every query head that
+// shares the K/V head (G > 1 for grouped-query attention) once, in tiles of 64.  Wave w owns keys
+// 32w .. 32w+31: their K and V rows stay in registers as MFMA B operands, and their fp32 dK^T,
+// dV^T accumulate in registers.  Per 32-query block:
+//   S   = Q K^T           A = Q rows (LDS),  B = K rows (registers)      -> lane = key
+//   D-dP = D + dO (-V)^T  A = dO rows (LDS), B = -V rows (registers), accumulators start at D
+//   P   = exp2(S*scale*log2e - lse_i*log2e),  -dS = P (D - dP)           (fp32)
+//   dV^T += dO^T P        A = dO^T by transposed LDS reads, B = P from registers
+//   -dK^T += Q^T (-dS)    A = Q^T by transposed LDS reads,  B = -dS from registers
+// (negating V and dK are exact, and let the matrix cores subtract D).
+//
+// With one wave per SIMD nothing hides a stall, so each wave runs a fixed schedule, software
+// pipelined over 32-query blocks: phase 1 of block j issues the 16 S/dP products of block j+1, one
+// at a time, each beside half of one of the P/dS elements 8..15 of block j; phase 2 issues the 16
+// dV/dK products of block j, each beside half of one of the elements 0..7 of block j+1.  LDS
+// operands are read 8 products ahead.  Every vector instruction then hides behind a matrix
+// product.  Q, dO, lse and D rotate through a four-stage LDS ring filled by direct global->LDS
+// loads three tiles ahead; one barrier per tile.  Rows past Nq in a head's last tile are clamped
+// copies whose dO row and D are zeroed in LDS, so they add nothing; key lanes past the chunk end
+// only feed their own dK/dV columns, which are not written.  dQ is computed by the
+// query-stationary kernel in bwd_dq_bf16.hip.
+//
+// Register files: the 128 dK^T/dV^T accumulators and the K/V fragments live in AGPRs (MFMA
+// accumulator and operand registers), the S/dP accumulators, P/dS and the operands in flight in
+// VGPRs.  The matrix products are inline assembly so that each operand sits in the file named
+// for it.  The compiler does not track hazards through inline assembly, so the schedule keeps
+// every MFMA result at least 20 wait states (issued instructions, or s_nop cycles) away from any
+// other instruction that reads or moves it, and every vector write of an operand at least 2 wait
+// states ahead of the product that reads it; the tests check both in the built code.
 
 #include "ringx_device.h"
 #include "ringx_kernels.h"
+
+#include <type_traits>
 
 namespace ringx {
 namespace {
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
+// The matrix products, volatile so that they keep the order the schedule gives them.
+// acc += A B with the accumulator in AGPRs
+__device__ __forceinline__ void mfma_acc_a(f32x16& acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// acc = A B (first product of a chain) and acc += A B, accumulator in VGPRs, B in AGPRs
+__device__ __forceinline__ void mfma_first_v(f32x16& acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));
+}
+// acc = A B + c (first product of a chain that starts from c)
+__device__ __forceinline__ void mfma_first_vc(f32x16& acc, bf16x8 a, bf16x8 b, const f32x16& c) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(acc) : "v"(a), "a"(b), "v"(c));
+}
+__device__ __forceinline__ void mfma_acc_v(f32x16& acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
+}
+
 template <int D>
 struct DkvCfg {
-  static constexpr int kThreads = 512;
-  static constexpr int kWaves = 8;
-  static constexpr int kBK = 128;                  // keys per workgroup (32 per key block)
-  static constexpr int kBQ = 8192 / D;             // queries per tile: 64 (d=128), 128 (d=64)
-  static constexpr int kQW = kBQ / 2;              // queries per wave
-  static constexpr int kQB = kQW / 32;             // 32-query blocks per wave
+  static constexpr int kThreads = 256;
+  static constexpr int kWaves = 4;
+  static constexpr int kBK = 128;                  // keys per workgroup (32 per wave)
+  static constexpr int kBQ = 64;                   // queries per tile
   static constexpr int kRowBytes = 2 * D;          // Q, dO, K, V rows
+  static constexpr int kChunks = D / 8;            // 16-byte chunks per row
   static constexpr int kDSteps = D / 16;
   static constexpr int kCT = D / 32;
-  static constexpr int kQTile = kBQ * kRowBytes;   // bytes of one Q or dO tile (16 KiB)
-  static constexpr int kKTile = kBK * kRowBytes;   // bytes of the K or V tile
-  // LDS carve-up (bytes)
-  static constexpr int kOffK = 0;
-  static constexpr int kOffV = kOffK + kKTile;
-  static constexpr int kOffQ = kOffV + kKTile;          // 2 buffers
-  static constexpr int kOffO = kOffQ + 2 * kQTile;      // 2 buffers
-  static constexpr int kOffL = kOffO + 2 * kQTile;      // 2 x kBQ floats: lse
-  static constexpr int kOffD = kOffL + 2 * kBQ * 4;     // 2 x kBQ floats: D
-  static constexpr int kLds = kOffD + 2 * kBQ * 4;
-  static_assert(kQB * 32 * 2 == kBQ, "two query halves");
-  static_assert(4 * kQTile >= kWaves / 2 * kCT * 16 * 64 * 4, "dK/dV exchange fits");
+  static constexpr int kQTile = kBQ * kRowBytes;   // bytes of one Q or dO tile
+  static constexpr int kLoads = kQTile / (kThreads * 16);   // 16-byte loads per thread per tile
+  // one stage of the ring: Q tile, dO tile, lse[kBQ], D[kBQ]
+  static constexpr int kOffO = kQTile;
+  static constexpr int kOffL = 2 * kQTile;
+  static constexpr int kOffD = kOffL + kBQ * 4;
+  static constexpr int kStage = kOffD + kBQ * 4;
+  static constexpr int kStages = 4;
+  static constexpr int kLds = kStages * kStage;
+  // vector-memory operations one tile puts in flight per wave (waves 0 and 1 add lse / D)
+  static constexpr int kTileOps = 2 * kLoads;
+  static_assert(kLoads >= 1 && kQTile == kLoads * kThreads * 16, "whole tiles per load round");
 };
 
 // XOR swizzle of the 16-byte chunks of a row of `RB` bytes (as in the forward kernel): 16
@@ -69,61 +103,44 @@ __device__ __forceinline__ int eoff(int row, int col) {
   return toff<RB>(row, col >> 3) + (col & 7) * 2;
 }
 
-// Rows row0 .. of a [N, D] bf16 matrix into a swizzled LDS tile at `dst` (rows clamped to
-// `last`), `per_wave` 1 KiB blocks per wave.
-template <int D>
-__device__ __forceinline__ void issue_rows(const __bf16* __restrict__ src, uint32_t dst,
-                                           int64_t row0, int64_t last, int per_wave, int wave,
-                                           int lane, int nwaves) {
-  constexpr int kCh = D / 8;
-  for (int u = 0; u < per_wave; ++u) {
-    const int blk = u * nwaves + wave;
-    const int slot = blk * 64 + lane;
-    const int row = slot / kCh;
-    const int c = (slot % kCh) ^ swz<2 * D>(row);
-    int64_t r = row0 + row;
-    r = r < last ? r : last;
-    load_lds16(src + r * D + c * 8, dst + (uint32_t)__builtin_amdgcn_readfirstlane(blk * 1024));
-  }
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone), n < 64.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// lse and D of queries row0 .. row0 + BQ - 1 (clamped to `last`) into LDS, 4 bytes per lane:
-// waves 0 and 1 load lse, waves 2 and 3 load D.
-template <int BQ>
-__device__ __forceinline__ void issue_rowvals(const float* __restrict__ lseb,
-                                              const float* __restrict__ deltab, uint32_t ldst,
-                                              uint32_t ddst, int64_t row0, int64_t last,
-                                              int wave, int lane) {
-  static_assert(BQ <= 128, "two waves per array");
-  const int part = wave & 1;
-  if (wave < 4 && part * 64 < BQ) {
-    int64_t r = row0 + part * 64 + lane;
-    r = r < last ? r : last;
-    if (wave < 2)
-      load_lds4(lseb + r, ldst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
-    else
-      load_lds4(deltab + r, ddst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
-  }
+// Direct global->LDS loads with a uniform 64-bit base in SGPRs and a per-lane 32-bit offset:
+// LDS destination = lds_base + 16 * lane (4 * lane for the dword form).
+__device__ __forceinline__ void load_lds16_s(const void* base, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(off), "s"(base)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void load_lds4_s(const void* base, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2"
+               :
+               : "s"(lds_base), "v"(off), "s"(base)
+               : "memory", "m0");
 }
 
 template <int D>
-__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ lse,
     const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BHkv,
-    int H, int grp,
-    int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale, int accumulate) {
+    int H, int grp, int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale,
+    int accumulate) {
   using C = DkvCfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds[C::kLds];
   const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int wave = t >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int n = lane & 31;
   const int g = lane >> 5;
-  const int kb = wave & 3;          // key block of this wave
-  const int qh = wave >> 2;         // query half of this wave
 
   const uint32_t wg = xcd_remap(blockIdx.x, gridDim.x);
   const int64_t per_bh = (int64_t)R * tiles_per_chunk;
@@ -135,52 +152,108 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   const int64_t hi = (int64_t)(r + 1) * Nk / R;
   const int64_t k0 = lo + (int64_t)tile * C::kBK;
   if (k0 >= hi) return;                         // uniform over the workgroup
-  const int nvalid = (int)min<int64_t>(C::kBK, hi - k0);
 
-  const __bf16* kbp = k + bh * Nk * D;
-  const __bf16* vbp = v + bh * Nk * D;
-  // the grp query heads sharing this K/V head are swept one after the other: query tile it is
-  // tile it % nqt of head qh0 + it / nqt
+  // the grp query heads sharing this K/V head are swept one after the other
   const int64_t qh0 = (bh / (H / grp)) * H + (bh % (H / grp)) * grp;
-  const __bf16* qb = q + qh0 * Nq * D;
-  const __bf16* ob = dout + qh0 * Nq * D;
+  const char* qb = reinterpret_cast<const char*>(q + qh0 * Nq * D);
+  const char* ob = reinterpret_cast<const char*>(dout + qh0 * Nq * D);
   const float* lseb = lse + qh0 * Nq;
   const float* deltab = delta + qh0 * Nq;
+  const int nqt = (int)((Nq + C::kBQ - 1) / C::kBQ);
+  const int ntiles = grp * nqt;
+  const int tail = (int)(Nq - (nqt - 1) * C::kBQ);   // valid rows of a head's last tile
 
-  const int64_t nqt = (Nq + C::kBQ - 1) / C::kBQ;
+  // Per-lane offsets of the tile loads: load round u covers rows 16 u + (wave * 64 + lane) / 16
+  // (d = 128) at a swizzled 16-byte chunk, so the offsets of round u are those of round 0 plus u
+  // times the round's bytes (the swizzle repeats every 16 rows).
+  constexpr uint32_t kRound = C::kWaves * 64 * 16;
+  static_assert(kRound % (16 * C::kRowBytes) == 0, "rounds keep the swizzle phase");
+  const int row0 = (wave * 64 + lane) / C::kChunks;
+  const uint32_t goff = row0 * C::kRowBytes +
+                        (((wave * 64 + lane) % C::kChunks) ^ swz<C::kRowBytes>(row0)) * 16;
+  const uint32_t wdst = (uint32_t)__builtin_amdgcn_readfirstlane(wave * 1024);
+  // next tile to load: first row within its head, and its row in the grp * Nq rows of the heads
+  int ld_r = 0;
+  int64_t ld_row = 0;
+  auto issue_next = [&](int stage) {
+    const char* qs = qb + ld_row * C::kRowBytes;
+    const char* os = ob + ld_row * C::kRowBytes;
+    const uint32_t dst = lbase + stage * C::kStage + wdst;
+    if (ld_r + C::kBQ <= Nq) {
+#pragma unroll
+      for (int u = 0; u < C::kLoads; ++u) {
+        load_lds16_s(qs + u * kRound, goff, dst + u * kRound);
+        load_lds16_s(os + u * kRound, goff, dst + C::kOffO + u * kRound);
+      }
+      if (wave == 0) load_lds4_s(lseb + ld_row, 4 * lane, dst - wdst + C::kOffL);
+      else if (wave == 1) load_lds4_s(deltab + ld_row, 4 * lane, dst - wdst + C::kOffD);
+    } else {
+      // a head's last tile: rows past Nq are clamped to Nq - 1
+      cold_path();
+      const int last = (int)(Nq - 1 - ld_r);
+#pragma unroll
+      for (int u = 0; u < C::kLoads; ++u) {
+        const int row = row0 + u * (kRound / C::kRowBytes);
+        const uint32_t off = goff + u * kRound - (row > last ? (row - last) * C::kRowBytes : 0);
+        load_lds16_s(qs, off, dst + u * kRound);
+        load_lds16_s(os, off, dst + C::kOffO + u * kRound);
+      }
+      const uint32_t loff = 4 * min(lane, last);
+      if (wave == 0) load_lds4_s(lseb + ld_row, loff, dst - wdst + C::kOffL);
+      else if (wave == 1) load_lds4_s(deltab + ld_row, loff, dst - wdst + C::kOffD);
+    }
+    ld_r += C::kBQ;
+    ld_row += C::kBQ;
+    if (ld_r >= Nq) {
+      ld_row += Nq - ld_r;   // next head
+      ld_r = 0;
+    }
+  };
+  // the first three query tiles in flight
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+    if (s < ntiles) issue_next(s);
 
-  // K and V tiles (kept for the whole sweep), then the first query tile
-  issue_rows<D>(kbp, lbase + C::kOffK, k0, hi - 1, C::kKTile / 1024 / C::kWaves, wave, lane,
-                C::kWaves);
-  issue_rows<D>(vbp, lbase + C::kOffV, k0, hi - 1, C::kKTile / 1024 / C::kWaves, wave, lane,
-                C::kWaves);
-  issue_rows<D>(qb, lbase + C::kOffQ, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
-                C::kWaves);
-  issue_rows<D>(ob, lbase + C::kOffO, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
-                C::kWaves);
-  issue_rowvals<C::kBQ>(lseb, deltab, lbase + C::kOffL, lbase + C::kOffD, 0, Nq - 1, wave, lane);
-  const float* lds_l = reinterpret_cast<const float*>(lds + C::kOffL);
-  const float* lds_d = reinterpret_cast<const float*>(lds + C::kOffD);
+  // this wave's 32 keys: K and V rows as B operands (key n, dims 16s + 8g .. +8)
+  const int64_t key = k0 + 32 * wave + n;
+  const bool key_ok = key < hi;
+  bf16x8 kf[C::kDSteps], vf[C::kDSteps];
+  {
+    const int64_t kr = key_ok ? key : hi - 1;
+    const __bf16* kp = k + (bh * Nk + kr) * D + 8 * g;
+    const __bf16* vp = v + (bh * Nk + kr) * D + 8 * g;
+#pragma unroll
+    for (int s = 0; s < C::kDSteps; ++s) {
+      kf[s] = *reinterpret_cast<const bf16x8*>(kp + 16 * s);
+      // -V: the dP products then start from D and return D - dP (exact sign flips)
+      vf[s] = __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4*>(vp + 16 * s) ^ (u32x4)0x80008000u);
+    }
+    // the fragments are in AGPRs, two wait states before the first product that reads them
+#pragma unroll
+    for (int s = 0; s < C::kDSteps; ++s) asm volatile("" : "+a"(kf[s]), "+a"(vf[s]));
+    asm volatile("s_nop 2");
+  }
 
-  // per-lane LDS byte offsets (tile-relative)
-  // S / dP: A = Q/dO rows (query qh*kQW + 32*b + n), B = K/V rows (key 32*kb + n); chunk 2s+g
+  // per-lane LDS byte offsets (stage-relative)
+  // S / dP: A = Q / dO rows (query 32b + n), chunk 2s + g
   int aoff[C::kDSteps];
 #pragma unroll
-  for (int s = 0; s < C::kDSteps; ++s) aoff[s] = toff<2 * D>(n, 2 * s + g);   // + row block
-  // transposed reads of Q/dO (rows = queries, cols = dims): 16-lane group G reads rows
-  // j0 + (lane%16)/4 with j0 = 4g + 8h (+16*ks), columns 32*ct + 16*(G&1) + 4*(lane%4); lane i
-  // of the group receives rows j0..j0+3 of column 32*ct + 16*(G&1) + i.
-  const int G = lane >> 4;
-  const int trr = (lane & 15) >> 2;
-  const int trc = 16 * (G & 1) + 4 * (lane & 3);
+  for (int s = 0; s < C::kDSteps; ++s) aoff[s] = toff<C::kRowBytes>(n, 2 * s + g);
+  // transposed reads of Q / dO (rows = queries, cols = dims): 16-lane group G reads rows
+  // j0 + (lane%16)/4 with j0 = 4g + 8h (+16 per query step), columns 32*ct + 16*(G&1) + 4*(lane%4);
+  // lane i of the group receives rows j0..j0+3 of column 32*ct + 16*(G&1) + i.
   int qtoff[2][C::kCT];
+  {
+    const int G = lane >> 4;
+    const int trr = (lane & 15) >> 2;
+    const int trc = 16 * (G & 1) + 4 * (lane & 3);
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int ct = 0; ct < C::kCT; ++ct)
-      qtoff[h][ct] = eoff<2 * D>(4 * g + 8 * h + trr, 32 * ct + trc);
-
-  const bool key_ok = 32 * kb + n < nvalid;
+      for (int ct = 0; ct < C::kCT; ++ct)
+        qtoff[h][ct] = eoff<C::kRowBytes>(4 * g + 8 * h + trr, 32 * ct + trc);
+  }
 
   f32x16 dvt[C::kCT], dkt[C::kCT];
 #pragma unroll
@@ -189,166 +262,239 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     dkt[c] = f32x16{};
   }
 
-  wait_vmem_all();
+  // Rows tail .. kBQ-1 of a head's last tile are clamped copies: a zero dO row and D make their
+  // P dO and dS vanish.  Called between barriers on a stage that has landed.
+  auto zero_tail = [&](int stage) {
+    char* ot = lds + stage * C::kStage + C::kOffO;
+    float* dd = reinterpret_cast<float*>(lds + stage * C::kStage + C::kOffD);
+    for (int i = t; i < (C::kBQ - tail) * C::kChunks; i += C::kThreads)
+      *reinterpret_cast<u32x4*>(ot + (tail + i / C::kChunks) * C::kRowBytes +
+                                (i % C::kChunks) * 16) = u32x4{};
+    if (t >= tail && t < C::kBQ) dd[t] = 0.f;
+  };
+  // position of the tile after the current one, within its head (first row)
+  int nx_r = 0;
+
+  wait_vmem<0>();
   __syncthreads();
-
-  const int64_t ntiles = (int64_t)grp * nqt;
-  int64_t q0 = 0;     // first row of the current tile within its head
-  int64_t qn = 0;     // first row of the next tile, and the offset (in rows) of its head
-  int64_t hn = 0;
-  for (int64_t it = 0; it < ntiles; ++it) {
-    const int cur = (int)(it & 1);
-    // next query tile in flight: Q, dO rows and their lse, D straight into LDS
-    qn = q0 + C::kBQ;
-    if (qn >= Nq) {
-      qn = 0;
-      hn += Nq;
-    }
-    if (it + 1 < ntiles) {
-      issue_rows<D>(qb + hn * D, lbase + C::kOffQ + (cur ^ 1) * C::kQTile, qn, Nq - 1,
-                    C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rows<D>(ob + hn * D, lbase + C::kOffO + (cur ^ 1) * C::kQTile, qn, Nq - 1,
-                    C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rowvals<C::kBQ>(lseb + hn, deltab + hn, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
-                            lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, qn, Nq - 1, wave, lane);
-    }
-    // last query tile (rows past Nq are clamped copies) or a partial key tile
-    const bool masked = q0 + C::kBQ > Nq || nvalid < C::kBK;
-    const char* qt = lds + C::kOffQ + cur * C::kQTile;
-    const char* ot = lds + C::kOffO + cur * C::kQTile;
-    const char* kt = lds + C::kOffK;
-    const char* vt = lds + C::kOffV;
-    const float* cl = lds_l + cur * C::kBQ;
-    const float* cd = lds_d + cur * C::kBQ;
-
-    // S = Q K^T, dP = dO V^T for this wave's 32 keys and kQW queries
-    f32x16 sacc[C::kQB], pacc[C::kQB];
-#pragma unroll
-    for (int b = 0; b < C::kQB; ++b) {
-      sacc[b] = f32x16{};
-      pacc[b] = f32x16{};
-    }
-#pragma unroll
-    for (int s = 0; s < C::kDSteps; ++s) {
-      const bf16x8 bk = *reinterpret_cast<const bf16x8*>(kt + (32 * kb) * C::kRowBytes + aoff[s]);
-      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(vt + (32 * kb) * C::kRowBytes + aoff[s]);
-#pragma unroll
-      for (int b = 0; b < C::kQB; ++b) {
-        const int rowb = (qh * C::kQW + 32 * b) * C::kRowBytes;
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(qt + rowb + aoff[s]);
-        const bf16x8 ao = *reinterpret_cast<const bf16x8*>(ot + rowb + aoff[s]);
-        sacc[b] = mfma32(aq, bk, sacc[b]);
-        pacc[b] = mfma32(ao, bv, pacc[b]);
-      }
-    }
-    // P and dS (fp32) -> bf16 B operands.  Accumulator r of block b is query
-    // 32b + 8(r/4) + 4g + r%4; the 8 queries of k-step 2b+h are accumulators 8h .. 8h+7.
-    // the vector work goes ahead of the other wave's matrix products on the SIMD
-    __builtin_amdgcn_s_setprio(1);
-    bf16x8 pf[2 * C::kQB], sf[2 * C::kQB];
-#pragma unroll
-    for (int b = 0; b < C::kQB; ++b) {
-      float p[16], dsv[16];
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int qi = qh * C::kQW + 32 * b + 8 * rq + 4 * g;   // 4 consecutive queries
-        const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + qi) * -kLog2e;
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(cd + qi);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float pe = fast_exp2(__builtin_fmaf(sacc[b][4 * rq + e], c2, nl4[e]));
-          p[4 * rq + e] = pe;
-          dsv[4 * rq + e] = pe * (pacc[b][4 * rq + e] - d4[e]);
-        }
-      }
-      if (masked) {
-        // keys past the chunk end (one lane each) and queries past Nq (clamped copies) add nothing
-        cold_path();
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int qi = qh * C::kQW + 32 * b + 8 * (rr >> 2) + 4 * g + (rr & 3);
-          if (!key_ok || q0 + qi >= Nq) {
-            p[rr] = 0.f;
-            dsv[rr] = 0.f;
-          }
-        }
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        u32x4 wp, ws;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          wp[e] = pack_bf16x2(p[8 * h + 2 * e], p[8 * h + 2 * e + 1]);
-          ws[e] = pack_bf16x2(dsv[8 * h + 2 * e], dsv[8 * h + 2 * e + 1]);
-        }
-        pf[2 * b + h] = __builtin_bit_cast(bf16x8, wp);
-        sf[2 * b + h] = __builtin_bit_cast(bf16x8, ws);
-      }
-    }
-    __builtin_amdgcn_s_setprio(0);
-    // dV^T += dO^T P, dK^T += Q^T dS
-#pragma unroll
-    for (int ks = 0; ks < 2 * C::kQB; ++ks) {
-      const int rowb = (qh * C::kQW + 16 * ks) * C::kRowBytes;
-#pragma unroll
-      for (int c = 0; c < C::kCT; ++c) {
-        const bf16x4 o0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + qtoff[0][c]));
-        const bf16x4 o1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + qtoff[1][c]));
-        const bf16x4 q0v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + qtoff[0][c]));
-        const bf16x4 q1v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + qtoff[1][c]));
-        dvt[c] = mfma32(__builtin_shufflevector(o0, o1, 0, 1, 2, 3, 4, 5, 6, 7), pf[ks], dvt[c]);
-        dkt[c] = mfma32(__builtin_shufflevector(q0v, q1v, 0, 1, 2, 3, 4, 5, 6, 7), sf[ks], dkt[c]);
-      }
-    }
-    // transposed Q / dO reads run ahead of the matrix products that consume them
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int i = 0; i < 4 * C::kQB * C::kCT; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    }
-    // next tile landed (the only vector memory operations in flight); this tile's reads done
-    wait_vmem_all();
+  if (tail < C::kBQ && nqt == 1) {
+    cold_path();
+    zero_tail(0);
     __syncthreads();
-    q0 = qn;
   }
 
-  // the two query halves of a key block add their dK^T / dV^T through LDS
-  float* xch = reinterpret_cast<float*>(lds + C::kOffQ);
-  const int64_t key = k0 + 32 * kb + n;
-  float* dkr = dk + (bh * Nk + key) * D;
-  float* dvr = dv + (bh * Nk + key) * D;
-#pragma unroll
-  for (int which = 0; which < 2; ++which) {
-    f32x16* acc = which == 0 ? dkt : dvt;
-    if (qh == 1) {
-#pragma unroll
-      for (int c = 0; c < C::kCT; ++c)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) xch[((kb * C::kCT + c) * 16 + rr) * 64 + lane] = acc[c][rr];
+  constexpr int kM1 = 2 * C::kDSteps;   // S and dP products of one block (phase 1)
+  constexpr int kM2 = 4 * C::kCT;       // dV and dK products of one block (phase 2)
+  constexpr int kEl = 16 / kM1;         // P/dS elements per phase-1 product
+  constexpr int kPf = 8;                // operand reads run this many products ahead
+  static_assert(kM1 >= kPf && kM2 >= kPf && kEl * kM1 == 16, "pipeline shape");
+
+  // operand reads, by product index:
+  // phase 1 product i: S (i even) or dP (i odd), k-step i/2, of the block at (st, blk)
+  auto read_a = [&](int i, int st, int blk) -> bf16x8 {
+    const char* base = lds + st + ((i & 1) ? C::kOffO : 0) + 32 * blk * C::kRowBytes;
+    return *reinterpret_cast<const bf16x8*>(base + aoff[i >> 1]);
+  };
+  // phase 2 product i: dV (i even, dO^T) or dK (i odd, Q^T), pair i/2 = (ks, c)
+  auto read_t = [&](int i, int st, int blk) -> bf16x8 {
+    const int p = i >> 1, ks = p / C::kCT, c = p % C::kCT;
+    const char* base = lds + st + ((i & 1) ? 0 : C::kOffO) + (32 * blk + 16 * ks) * C::kRowBytes;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + qtoff[0][c]));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + qtoff[1][c]));
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  auto read_l = [&](int rq, int st, int blk, f32x4& l4) {
+    const float* cl = reinterpret_cast<const float*>(lds + st + C::kOffL) + 32 * blk + 8 * rq + 4 * g;
+    l4 = *reinterpret_cast<const f32x4*>(cl);
+  };
+  // D of a block in accumulator order (element 4 rq + x is query 8 rq + 4 g + x)
+  auto read_d = [&](int st, int blk) -> f32x16 {
+    const float* cd = reinterpret_cast<const float*>(lds + st + C::kOffD) + 32 * blk + 4 * g;
+    const f32x4 d0 = *reinterpret_cast<const f32x4*>(cd);
+    const f32x4 d1 = *reinterpret_cast<const f32x4*>(cd + 8);
+    const f32x4 d2 = *reinterpret_cast<const f32x4*>(cd + 16);
+    const f32x4 d3 = *reinterpret_cast<const f32x4*>(cd + 24);
+    return __builtin_shufflevector(__builtin_shufflevector(d0, d1, 0, 1, 2, 3, 4, 5, 6, 7),
+                                   __builtin_shufflevector(d2, d3, 0, 1, 2, 3, 4, 5, 6, 7), 0, 1,
+                                   2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
+  };
+
+  bf16x8 abuf[kM1];                 // phase-1 A operands in flight (indexed by product)
+  bf16x8 tbuf[kM2];                 // phase-2 A operands in flight
+  f32x4 lbuf[4];                    // lse of 4-query groups rq of the blocks in flight
+  f32x16 dblk;                      // D of the block whose dP products come next
+
+  // P and dS of score element e of a block, in two halves of about equal issue cost: the
+  // exponential (reads S), then dS and the packing (reads dP).  pw, sw collect the packed pairs.
+  float pe[16], dse[16];
+  auto elem_exp = [&](const f32x16& cs, int e) {
+    float se = cs[e];
+    asm volatile("" : "+v"(se));
+    pe[e] = fast_exp2(__builtin_fmaf(se, c2, lbuf[e >> 2][e & 3] * -kLog2e));
+  };
+  auto elem_ds = [&](const f32x16& cp, int e, u32x4& pw, u32x4& sw) {
+    float dpe = cp[e];                        // D - dP
+    asm volatile("" : "+v"(dpe));
+    dse[e] = pe[e] * dpe;                     // -dS
+    if (e & 1) {
+      uint32_t a2 = pack_bf16x2(pe[e - 1], pe[e]), b2 = pack_bf16x2(dse[e - 1], dse[e]);
+      asm volatile("" : "+v"(a2), "+v"(b2));
+      pw[(e & 7) >> 1] = a2;
+      sw[(e & 7) >> 1] = b2;
     }
-    __syncthreads();
-    if (qh == 0) {
+  };
+
+  // Phase 1 of block j at (st, blk), scores (cs, cp): the S/dP products of block j+1 (at
+  // (st_n, blk_n)) into (ns, np), each beside half of one of the score elements 8..15 of block j
+  // (into pf1, sf1).  The last kPf slots start this block's phase-2 reads; lse and D of block j+1's
+  // first two query groups are read on the way.
+  auto phase1 = [&](const f32x16& cs, const f32x16& cp, f32x16& ns, f32x16& np, bf16x8& pf1,
+                    bf16x8& sf1, int st, int blk, int st_n, int blk_n) {
+    u32x4 pw, sw;
 #pragma unroll
-      for (int c = 0; c < C::kCT; ++c)
+    for (int i = 0; i < kM1; ++i) {
+      if (i + kPf < kM1) abuf[i + kPf] = read_a(i + kPf, st_n, blk_n);
+      else tbuf[i + kPf - kM1] = read_t(i + kPf - kM1, st, blk);
+      if (i == 1 || i == 3) read_l(i >> 1, st_n, blk_n, lbuf[i >> 1]);
+      f32x16& acc = (i & 1) ? np : ns;
+      const bf16x8 bop = (i & 1) ? vf[i >> 1] : kf[i >> 1];
+      if (i == 0) mfma_first_v(acc, abuf[i], bop);
+      else if (i == 1) mfma_first_vc(acc, abuf[i], bop, dblk);
+      else mfma_acc_v(acc, abuf[i], bop);
 #pragma unroll
-        for (int rr = 0; rr < 16; ++rr) acc[c][rr] += xch[((kb * C::kCT + c) * 16 + rr) * 64 + lane];
-      if (key_ok) {
-        float* dst = which == 0 ? dkr : dvr;
-        const float f = which == 0 ? scale : 1.0f;
-#pragma unroll
-        for (int c = 0; c < C::kCT; ++c)
-#pragma unroll
-          for (int rq = 0; rq < 4; ++rq) {
-            const int col = c * 32 + 8 * rq + 4 * g;
-            f32x4 val = {acc[c][4 * rq] * f, acc[c][4 * rq + 1] * f, acc[c][4 * rq + 2] * f,
-                         acc[c][4 * rq + 3] * f};
-            if (accumulate) val += *reinterpret_cast<const f32x4*>(dst + col);
-            *reinterpret_cast<f32x4*>(dst + col) = val;
-          }
+      for (int u = 0; u < kEl; ++u) {
+        const int h = i * kEl + u;            // half-element index 0 .. 15
+        const int e = 8 + (h >> 1);
+        if (h & 1) elem_ds(cp, e, pw, sw);
+        else elem_exp(cs, e);
       }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    pf1 = __builtin_bit_cast(bf16x8, pw);
+    sf1 = __builtin_bit_cast(bf16x8, sw);
+  };
+  // Phase 2 of block j at (st, blk): its dV/dK products with (pf, sf), each beside half of one of
+  // the score elements 0..7 of block j+1 (scores (ns, np), into pfn0, sfn0), starting one product
+  // late so that the S/dP products just issued have finished.  The last kPf slots start the reads
+  // of the next phase 1 (A operands of block j+2 at (st_a, blk_a)); lse and D of block j+1's last
+  // two query groups (at (st_n, blk_n)) are read on the way.
+  auto phase2 = [&](const bf16x8 (&pf)[2], const bf16x8 (&sf)[2], const f32x16& ns,
+                    const f32x16& np, bf16x8& pfn0, bf16x8& sfn0, int st, int blk, int st_n,
+                    int blk_n, int st_a, int blk_a) {
+    u32x4 pw, sw;
+    constexpr int kH = 16 / kM2;              // half-elements per product
+#pragma unroll
+    for (int i = 0; i < kM2; ++i) {
+      if (i + kPf < kM2) {
+        tbuf[i + kPf] = read_t(i + kPf, st, blk);
+      } else {
+        const int k2 = i + kPf - kM2;
+        abuf[k2] = read_a(k2, st_a, blk_a);
+        if (k2 == 1) dblk = read_d(st_a, blk_a);
+      }
+      if (i == 1 || i == 3) read_l(2 + (i >> 1), st_n, blk_n, lbuf[2 + (i >> 1)]);
+      const int c = (i >> 1) % C::kCT, ks = (i >> 1) / C::kCT;
+      if (i & 1) mfma_acc_a(dkt[c], tbuf[i], sf[ks]);
+      else mfma_acc_a(dvt[c], tbuf[i], pf[ks]);
+#pragma unroll
+      for (int u = 0; u < kH; ++u) {
+        const int h = i * kH + u - 1;         // half-element index, one product late
+        if (h >= 0) {
+          const int e = h >> 1;
+          if (h & 1) elem_ds(np, e, pw, sw);
+          else elem_exp(ns, e);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    elem_ds(np, 7, pw, sw);
+    pfn0 = __builtin_bit_cast(bf16x8, pw);
+    sfn0 = __builtin_bit_cast(bf16x8, sw);
+  };
+
+  // Block 0 of every tile lives in (sa, pa, pfa, sfa), block 1 in (sb, pb, pfb, sfb).
+  // Prologue: scores of block 0 of tile 0, its elements 0..7, and the reads of its phase 1.
+  f32x16 sa, pa, sb, pb;
+  bf16x8 pfa[2], sfa[2], pfb[2], sfb[2];
+  dblk = read_d(0, 0);
+#pragma unroll
+  for (int i = 0; i < kM1; ++i) {
+    f32x16& acc = (i & 1) ? pa : sa;
+    const bf16x8 aop = read_a(i, 0, 0);
+    const bf16x8 bop = (i & 1) ? vf[i >> 1] : kf[i >> 1];
+    if (i == 0) mfma_first_v(acc, aop, bop);
+    else if (i == 1) mfma_first_vc(acc, aop, bop, dblk);
+    else mfma_acc_v(acc, aop, bop);
+  }
+#pragma unroll
+  for (int rq = 0; rq < 4; ++rq) read_l(rq, 0, 0, lbuf[rq]);
+  // the vector ALU reads these scores next: their products have left the matrix cores by then
+  asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sa), "+v"(pa));
+  {
+    u32x4 pw, sw;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      elem_exp(sa, e);
+      elem_ds(pa, e, pw, sw);
+    }
+    pfa[0] = __builtin_bit_cast(bf16x8, pw);
+    sfa[0] = __builtin_bit_cast(bf16x8, sw);
+  }
+#pragma unroll
+  for (int k2 = 0; k2 < kPf; ++k2) abuf[k2] = read_a(k2, 0, 1);
+  dblk = read_d(0, 1);
+  __builtin_amdgcn_sched_barrier(0);
+
+  for (int it = 0; it < ntiles; ++it) {
+    const int st_cur = (int)(it & 3) * C::kStage;
+    const int st_nxt = (int)((it + 1) & 3) * C::kStage;
+    // tile it+1 landed (tile it+2 may stay in flight); every wave is done with tile it-1
+    if (it + 2 < ntiles) {
+      if (wave < 2) wait_vmem<C::kTileOps + 1>();
+      else wait_vmem<C::kTileOps>();
+    } else {
+      wait_vmem<0>();
     }
     __syncthreads();
+    nx_r += C::kBQ;
+    if (nx_r >= Nq) nx_r = 0;
+    if (it + 1 < ntiles && nx_r + C::kBQ > Nq) {
+      cold_path();
+      zero_tail((int)((it + 1) & 3));
+      __syncthreads();
+    }
+    if (it + 3 < ntiles) issue_next((int)((it + 3) & 3));
+    __builtin_amdgcn_sched_barrier(0);
+
+    // block 0 of tile it; block 1 of tile it next; then block 0 of tile it+1 (a stale stage after
+    // the last tile, whose results are not used)
+    phase1(sa, pa, sb, pb, pfa[1], sfa[1], st_cur, 0, st_cur, 1);
+    phase2(pfa, sfa, sb, pb, pfb[0], sfb[0], st_cur, 0, st_cur, 1, st_nxt, 0);
+    phase1(sb, pb, sa, pa, pfb[1], sfb[1], st_cur, 1, st_nxt, 0);
+    phase2(pfb, sfb, sa, pa, pfa[0], sfa[0], st_cur, 1, st_nxt, 0, st_nxt, 1);
+    // after the last products, before any code at the loop exit reads or moves the accumulators
+    if (it + 1 == ntiles) asm volatile("s_nop 15\n\ts_nop 15");
+  }
+
+  if (key_ok) {
+    float* dkr = dk + (bh * Nk + key) * D;
+    float* dvr = dv + (bh * Nk + key) * D;
+#pragma unroll
+    for (int c = 0; c < C::kCT; ++c)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int col = c * 32 + 8 * rq + 4 * g;
+        // the dK^T accumulators hold sums of -dS products
+        f32x4 kv = {dkt[c][4 * rq] * -scale, dkt[c][4 * rq + 1] * -scale,
+                    dkt[c][4 * rq + 2] * -scale, dkt[c][4 * rq + 3] * -scale};
+        f32x4 vv = {dvt[c][4 * rq], dvt[c][4 * rq + 1], dvt[c][4 * rq + 2], dvt[c][4 * rq + 3]};
+        if (accumulate) {
+          kv += *reinterpret_cast<const f32x4*>(dkr + col);
+          vv += *reinterpret_cast<const f32x4*>(dvr + col);
+        }
+        *reinterpret_cast<f32x4*>(dkr + col) = kv;
+        *reinterpret_cast<f32x4*>(dvr + col) = vv;
+      }
   }
 }
 
@@ -361,8 +507,8 @@ hipError_t launch(const BwdArgs& a) {
   hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
                      (const __bf16*)a.dout, a.lse, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
-                     (int)a.H, (int)a.G, a.Nq, a.Nk,
-                     (int)a.R, (int)tpc, a.scale * kLog2e, a.scale, a.accumulate_dkv ? 1 : 0);
+                     (int)a.H, (int)a.G, a.Nq, a.Nk, (int)a.R, (int)tpc, a.scale * kLog2e,
+                     a.scale, a.accumulate_dkv ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -370,7 +516,7 @@ hipError_t launch(const BwdArgs& a) {
 
 hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a) {
   if (a.d == 128) return launch<128>(a);
-  return launch<64>(a);
+  return launch_bwd_dkdv_bf16_d64(a);
 }
 
 }  // namespace ringx
