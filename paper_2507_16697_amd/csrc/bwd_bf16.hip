@@ -44,23 +44,6 @@ namespace {
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-// The matrix products, volatile so that they keep the order the schedule gives them.
-// acc += A B with the accumulator in AGPRs
-__device__ __forceinline__ void mfma_acc_a(f32x16& acc, bf16x8 a, bf16x8 b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-// acc = A B (first product of a chain) and acc += A B, accumulator in VGPRs, B in AGPRs
-__device__ __forceinline__ void mfma_first_v(f32x16& acc, bf16x8 a, bf16x8 b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));
-}
-// acc = A B + c (first product of a chain that starts from c)
-__device__ __forceinline__ void mfma_first_vc(f32x16& acc, bf16x8 a, bf16x8 b, const f32x16& c) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(acc) : "v"(a), "a"(b), "v"(c));
-}
-__device__ __forceinline__ void mfma_acc_v(f32x16& acc, bf16x8 a, bf16x8 b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
-}
-
 template <int D>
 struct DkvCfg {
   static constexpr int kThreads = 256;
@@ -101,28 +84,6 @@ __device__ __forceinline__ int toff(int row, int c) {
 template <int RB>
 __device__ __forceinline__ int eoff(int row, int col) {
   return toff<RB>(row, col >> 3) + (col & 7) * 2;
-}
-
-// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone), n < 64.
-template <int N>
-__device__ __forceinline__ void wait_vmem() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Direct global->LDS loads with a uniform 64-bit base in SGPRs and a per-lane 32-bit offset:
-// LDS destination = lds_base + 16 * lane (4 * lane for the dword form).
-__device__ __forceinline__ void load_lds16_s(const void* base, uint32_t off, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :
-               : "s"(lds_base), "v"(off), "s"(base)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void load_lds4_s(const void* base, uint32_t off, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2"
-               :
-               : "s"(lds_base), "v"(off), "s"(base)
-               : "memory", "m0");
 }
 
 template <int D>

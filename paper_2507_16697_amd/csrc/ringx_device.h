@@ -91,7 +91,58 @@ __device__ __forceinline__ void load_lds4(const void* gptr, uint32_t lds_base) {
                : "s"(lds_base), "v"(gptr)
                : "memory", "m0");
 }
+// A wave-uniform pointer in SGPRs (free when the compiler already holds it there).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t x = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return reinterpret_cast<const void*>(((uint64_t)hi << 32) | lo);
+}
+// The same loads with a uniform 64-bit base (the callers' base is the same for every lane) in
+// SGPRs and a per-lane 32-bit offset: the scalar-base form, no per-lane 64-bit address arithmetic.
+__device__ __forceinline__ void load_lds16_s(const void* base, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(off), "s"(uniform_ptr(base))
+               : "memory", "m0");
+}
+__device__ __forceinline__ void load_lds4_s(const void* base, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2"
+               :
+               : "s"(lds_base), "v"(off), "s"(uniform_ptr(base))
+               : "memory", "m0");
+}
+
+// v_mfma_f32_32x32x16_bf16 as inline assembly that names the register file of every operand ("a":
+// AGPRs, the matrix cores' accumulation/operand registers; "v": VGPRs), for kernels that need
+// more than the 256 VGPRs of one wave.  Volatile, so they keep the order the kernel gives them.
+// The compiler inserts no wait states around inline assembly: a kernel using these keeps every
+// result away from its next reader, and every vector write away from the product reading it
+// (tests/test_build_isa.py checks the built code).
+// acc += A B, accumulator in AGPRs
+__device__ __forceinline__ void mfma_acc_a(f32x16& acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// acc = A B (first product of a chain), accumulator in VGPRs, B in AGPRs
+__device__ __forceinline__ void mfma_first_v(f32x16& acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(acc) : "v"(a), "a"(b));
+}
+// acc = A B + c (first product of a chain that starts from c)
+__device__ __forceinline__ void mfma_first_vc(f32x16& acc, bf16x8 a, bf16x8 b, const f32x16& c) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(acc) : "v"(a), "a"(b), "v"(c));
+}
+// acc += A B, accumulator in VGPRs, B in AGPRs
+__device__ __forceinline__ void mfma_acc_v(f32x16& acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(acc) : "v"(a), "a"(b));
+}
 #pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left alone), n < 64.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
 // Keeps a rarely taken branch a branch: an empty volatile asm statement has side effects, so the
 // compiler cannot speculate the branch body into straight-line selects executed on every tile.

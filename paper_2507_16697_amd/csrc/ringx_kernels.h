@@ -83,6 +83,7 @@ hipError_t launch_bwd_pre(const BwdArgs& a, bool bf16);
 hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a);
 hipError_t launch_bwd_dkdv_bf16_d64(const BwdArgs& a);   // d = 64 (bwd_bf16_d64.hip)
 hipError_t launch_bwd_dq_bf16(const BwdArgs& a);
+hipError_t launch_bwd_dq_bf16_d64(const BwdArgs& a);   // d = 64 (bwd_dq_bf16_d64.hip)
 hipError_t launch_bwd_dkdv_f32(const BwdArgs& a);
 hipError_t launch_bwd_dq_f32(const BwdArgs& a);
 

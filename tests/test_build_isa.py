@@ -24,7 +24,8 @@ def _asm(src, tmp_path):
     return out.read_text()
 
 
-@pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip"])
+@pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip", "bwd_dq_bf16.hip",
+                                 "bwd_dq_bf16_d64.hip"])
 def test_m0_only_feeds_direct_lds_loads(src, tmp_path):
     lines = [l.strip() for l in _asm(src, tmp_path).splitlines()]
     code = [l for l in lines if l and not l.startswith(";") and not l.startswith(".")]
@@ -37,8 +38,8 @@ def test_m0_only_feeds_direct_lds_loads(src, tmp_path):
         assert re.match(r"global_load_lds_dword(x4)? ", code[i + 2]), code[i + 2]
 
 
-@pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip", "merge.hip",
-                                 "bwd_pre.hip"])
+@pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip", "bwd_dq_bf16.hip",
+                                 "bwd_dq_bf16_d64.hip", "merge.hip", "bwd_pre.hip"])
 def test_no_packed_fp32_and_no_scalar_stores(src, tmp_path):
     text = _asm(src, tmp_path)
     assert not re.search(r"\bv_pk_(add|mul|fma)_f32\b", text)
@@ -99,8 +100,10 @@ def mfma_hazards(code, window=96):
         w = 0
         for j in range(i - 1, max(-1, i - 16), -1):
             op2, ops2 = _split(code[j])
-            if op2.startswith("v_") and not op2.startswith("v_mfma") and ops2 and _regs(ops2[0]) & srcs:
-                near_write = w if near_write is None else min(near_write, w)
+            if ops2 and not op2.startswith(("s_", "v_mfma")) and _regs(ops2[0]) & srcs:
+                # the operand's last writer: a hazard only for the vector ALU (loads are waited on)
+                if op2.startswith("v_"):
+                    near_write = w if near_write is None else min(near_write, w)
                 break
             w += _waits(code[j])
     return near_result, near_write
@@ -131,18 +134,22 @@ def test_hazard_check_catches_close_accesses():
     # the next product of the same chain may follow at once; a new chain over it may not
     assert mfma_hazards([first, mfma, mfma])[0] is None
     assert mfma_hazards([mfma, first])[0] == 0
-    # an operand written by the vector ALU right before the product, and 2 wait states before it
+    # an operand written by the vector ALU right before the product, and 2 wait states before it;
+    # a load that overwrites the operand after the vector write ends the search
     assert mfma_hazards(["v_xor_b32 v17, v1, v2", mfma])[1] == 0
+    assert mfma_hazards(["v_add_u32 v16, v1, v2", "ds_read_b128 v[16:19], v16", mfma])[1] is None
     assert mfma_hazards(["v_accvgpr_write_b32 a2, v9", "s_nop 1", mfma])[1] == 2
     assert mfma_hazards(["v_accvgpr_write_b32 a2, v9", "s_nop 0", mfma])[1] == 1
 
 
-def test_dkdv_inline_mfma_spacing(tmp_path):
-    bodies = _kernel_bodies(_asm("bwd_bf16.hip", tmp_path))
-    kernels = [(name, code) for name, code in bodies if "bwd_dkdv_kernel" in name]
+@pytest.mark.parametrize("src,kernel,products", [("bwd_bf16.hip", "bwd_dkdv_kernel", 80),
+                                                  ("bwd_dq_bf16.hip", "bwd_dq_kernel", 128)])
+def test_inline_mfma_spacing(src, kernel, products, tmp_path):
+    bodies = _kernel_bodies(_asm(src, tmp_path))
+    kernels = [(name, code) for name, code in bodies if kernel in name]
     assert len(kernels) == 1, [n for n, _ in bodies]          # d = 128
     for name, code in kernels:
-        assert sum(1 for c in code if c.startswith("v_mfma")) >= 80, name
+        assert sum(1 for c in code if c.startswith("v_mfma")) >= products, name
         near_result, near_write = mfma_hazards(code)
         assert near_result is not None and near_result >= MFMA_RESULT_WAIT, (name, near_result)
         assert near_write is None or near_write >= VALU_TO_MFMA_WAIT, (name, near_write)
