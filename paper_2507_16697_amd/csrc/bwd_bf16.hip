@@ -265,7 +265,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
   auto read_l = [&](int rq, int st, int blk, f32x4& l4) {
-    const float* cl = reinterpret_cast<const float*>(lds + st + C::kOffL) + 32 * blk + 8 * rq + 4 * g;
+    const float* cl =
+        reinterpret_cast<const float*>(lds + st + C::kOffL) + 32 * blk + 8 * rq + 4 * g;
     l4 = *reinterpret_cast<const f32x4*>(cl);
   };
   // D of a block in accumulator order (element 4 rq + x is query 8 rq + 4 g + x)

@@ -21,9 +21,11 @@
 // unit u issues the 32 S/dP products of unit u+1, beside the P/dS arithmetic of three of the four
 // 8-element groups of unit u; phase 2 issues the 16 dQ products of unit u, beside the first group
 // of unit u+1 (started a few products late, so that the S/dP products just issued have
-// finished).  LDS operands are read 8 products ahead.  Key rows past the end of a chunk (last tile
-// of a chunk) are clamped copies, zeroed in the K stage once they land: their dS then meets a zero
-// K^T row and adds nothing, so the loop has no masking.
+// finished).  A product slot carries at most one element (fma, exp, subtract, multiply, half a
+// pack): one hides behind the 32-cycle product, two do not.  LDS operands are read 8 products
+// ahead.  Key rows past the end of a chunk (last tile of a chunk) are clamped copies, zeroed in the
+// K stage once they land: their dS then meets a zero K^T row and adds nothing, so the loop has no
+// masking.
 //
 // Register files: Q/dO fragments (128) and the dQ^T accumulators (128) in AGPRs, the S/dP
 // accumulators of two units, dS^T and the operands in flight in VGPRs; the products are the
@@ -231,7 +233,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     const char* base = lds + st + ((i & 2) ? C::kTile : 0) + 32 * kbk * C::kRowBytes;
     return *reinterpret_cast<const bf16x8*>(base + koff[i >> 2]);
   };
-  // Phase 2 product j: query block j % 2, pair j / 2 = (ks, c); A = K^T of keys 16 ks .. of the unit
+  // Phase 2 product j: query block j % 2, pair j / 2 = (ks, c); A = K^T of the unit's keys
+  // 16 ks .. 16 ks + 15
   auto read_t = [&](int j, int st, int kbk) -> bf16x8 {
     const int p = j >> 1, ks = p / C::kCT, c = p % C::kCT;
     const char* base = lds + st + (32 * kbk + 16 * ks) * C::kRowBytes;
@@ -243,32 +246,31 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
   bf16x8 abuf[kM1 / 2];             // phase-1 A operands in flight (one per product pair)
   bf16x8 tbuf[kM2 / 2];             // phase-2 A operands in flight
 
-  // P/dS of one score element, in two halves: the exponential (reads S), then dS and the packing
-  // (reads dP).  Element e of group G = (query block b, k-step ks) is accumulator 8 ks + e of b.
-  float pe[2][16];
-  auto half_elem = [&](const f32x16 (&sc)[2], const f32x16 (&dp)[2], int hidx, u32x4 (&sw)[2][2]) {
-    const int grp_i = hidx >> 4, e8 = (hidx >> 1) & 7;   // group, element within the group
-    const int b = grp_i == 1 || grp_i == 3 ? 1 : 0, ks = grp_i >> 1;
+  // P/dS of score element k (0 .. 31) of a unit: group k / 8 = (query block b, k-step ks), element
+  // 8 ks + k % 8 of b's accumulators.  Pairs are packed as dS^T B operands after their second
+  // element.
+  float dse[2][16];
+  auto elem = [&](const f32x16 (&sc)[2], const f32x16 (&dp)[2], int k, u32x4 (&sw)[2][2]) {
+    const int grp_i = k >> 3, e8 = k & 7;
+    const int b = grp_i & 1, ks = grp_i >> 1;
     const int e = 8 * ks + e8;
-    if ((hidx & 1) == 0) {
-      float se = sc[b][e];
-      asm volatile("" : "+v"(se));
-      pe[b][e] = fast_exp2(__builtin_fmaf(se, c2, nl[b]));
-    } else if (e8 & 1) {
-      float d0 = dp[b][e - 1], d1 = dp[b][e];
-      asm volatile("" : "+v"(d0), "+v"(d1));
-      uint32_t a2 = pack_bf16x2(pe[b][e - 1] * (d0 - dd[b]), pe[b][e] * (d1 - dd[b]));
+    float se = sc[b][e], de = dp[b][e];
+    asm volatile("" : "+v"(se), "+v"(de));
+    const float pe = fast_exp2(__builtin_fmaf(se, c2, nl[b]));
+    dse[b][e] = pe * (de - dd[b]);
+    if (e8 & 1) {
+      uint32_t a2 = pack_bf16x2(dse[b][e - 1], dse[b][e]);
       asm volatile("" : "+v"(a2));
       sw[b][ks][e8 >> 1] = a2;
     }
   };
 
   // Phase 1 of unit u (stage st, key block kbk; scores sc, dp) computes the S/dP of unit u+1 (at
-  // (st_n, kbk_n)) into (nsc, ndp), beside half-elements 16 .. 63 of unit u (groups 1..3) into sw;
-  // its last kPf slots start unit u's phase-2 reads.
+  // (st_n, kbk_n)) into (nsc, ndp), beside elements 8 .. 31 of unit u (groups 1..3) into sw, at
+  // most one per product; its last kPf slots start unit u's phase-2 reads.
   auto phase1 = [&](const f32x16 (&sc)[2], const f32x16 (&dp)[2], f32x16 (&nsc)[2],
                     f32x16 (&ndp)[2], u32x4 (&sw)[2][2], int st, int kbk, int st_n, int kbk_n) {
-    constexpr int kH = 48;            // half-elements carried by this phase
+    constexpr int kE = 24;            // elements carried by this phase
 #pragma unroll
     for (int i = 0; i < kM1; ++i) {
       if (((i + kPf) & 1) == 0) {
@@ -282,12 +284,12 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
       if (s == 0) mfma_first_v(acc, abuf[i >> 1], bop);
       else mfma_acc_v(acc, abuf[i >> 1], bop);
 #pragma unroll
-      for (int h = (i * kH) / kM1; h < ((i + 1) * kH) / kM1; ++h) half_elem(sc, dp, 16 + h, sw);
+      for (int e = (i * kE) / kM1; e < ((i + 1) * kE) / kM1; ++e) elem(sc, dp, 8 + e, sw);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
   // Phase 2 of unit u (stage st, key block kbk): its dQ products with B operands sf, beside
-  // half-elements 0 .. 15 of unit u+1 (group 0, scores nsc/ndp) into nsw, from product kLate on;
+  // elements 0 .. 7 of unit u+1 (group 0, scores nsc/ndp) into nsw, from product kLate on;
   // its last kPf slots start the reads of unit u+1's phase 1 (A operands of unit u+2 at
   // (st_a, kbk_a)).
   auto phase2 = [&](const bf16x8 (&sf)[2][2], const f32x16 (&nsc)[2], const f32x16 (&ndp)[2],
@@ -304,8 +306,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
       if (j >= kLate) {
         const int i2 = j - kLate;
 #pragma unroll
-        for (int h = (i2 * 16) / kSlots; h < ((i2 + 1) * 16) / kSlots; ++h)
-          half_elem(nsc, ndp, h, nsw);
+        for (int e = (i2 * 8) / kSlots; e < ((i2 + 1) * 8) / kSlots; ++e) elem(nsc, ndp, e, nsw);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -334,7 +335,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
   }
   asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sa[0]), "+v"(sa[1]), "+v"(pa[0]), "+v"(pa[1]));
 #pragma unroll
-  for (int h = 0; h < 16; ++h) half_elem(sa, pa, h, swa);
+  for (int e = 0; e < 8; ++e) elem(sa, pa, e, swa);
 #pragma unroll
   for (int i = 0; i < kPf; i += 2) abuf[i >> 1] = read_a(i, 0, 1);
   __builtin_amdgcn_sched_barrier(0);
