@@ -19,7 +19,7 @@
 // pipelined over 32-query blocks: phase 1 of block j issues the 16 S/dP products of block j+1, one
 // at a time, each beside half of one of the P/dS elements 8..15 of block j; phase 2 issues the 16
 // dV/dK products of block j, each beside half of one of the elements 0..7 of block j+1.  LDS
-// operands are read 8 products ahead.  Every vector instruction then hides behind a matrix
+// operands are read 16 products ahead.  Every vector instruction then hides behind a matrix
 // product.  Q, dO, lse and D rotate through a four-stage LDS ring filled by direct global->LDS
 // loads three tiles ahead; one barrier per tile.  Rows past Nq in a head's last tile are clamped
 // copies whose dO row and D are zeroed in LDS, so they add nothing; key lanes past the chunk end
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
   constexpr int kM1 = 2 * C::kDSteps;   // S and dP products of one block (phase 1)
   constexpr int kM2 = 4 * C::kCT;       // dV and dK products of one block (phase 2)
   constexpr int kEl = 16 / kM1;         // P/dS elements per phase-1 product
-  constexpr int kPf = 8;                // operand reads run this many products ahead
+  constexpr int kPf = 16;               // operand reads run this many products ahead
   static_assert(kM1 >= kPf && kM2 >= kPf && kEl * kM1 == 16, "pipeline shape");
 
   // operand reads, by product index:
@@ -336,7 +336,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     sf1 = __builtin_bit_cast(bf16x8, sw);
   };
   // Phase 2 of block j at (st, blk): its dV/dK products with (pf, sf), each beside half of one of
-  // the score elements 0..7 of block j+1 (scores (ns, np), into pfn0, sfn0), starting one product
+  // the score elements 0..7 of block j+1 (scores (ns, np), into pfn0, sfn0), starting two products
   // late so that the S/dP products just issued have finished.  The last kPf slots start the reads
   // of the next phase 1 (A operands of block j+2 at (st_a, blk_a)); lse and D of block j+1's last
   // two query groups (at (st_n, blk_n)) are read on the way.
@@ -360,7 +360,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
       else mfma_acc_a(dvt[c], tbuf[i], pf[ks]);
 #pragma unroll
       for (int u = 0; u < kH; ++u) {
-        const int h = i * kH + u - 1;         // half-element index, one product late
+        const int h = i * kH + u - 2;         // half-element index, two products late
         if (h >= 0) {
           const int e = h >> 1;
           if (h & 1) elem_ds(np, e, pw, sw);
@@ -369,6 +369,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    elem_exp(ns, 7);
     elem_ds(np, 7, pw, sw);
     pfn0 = __builtin_bit_cast(bf16x8, pw);
     sfn0 = __builtin_bit_cast(bf16x8, sw);

@@ -145,7 +145,12 @@ def test_hazard_check_catches_close_accesses():
 @pytest.mark.parametrize("src,kernel,products", [("bwd_bf16.hip", "bwd_dkdv_kernel", 80),
                                                   ("bwd_dq_bf16.hip", "bwd_dq_kernel", 128)])
 def test_inline_mfma_spacing(src, kernel, products, tmp_path):
-    bodies = _kernel_bodies(_asm(src, tmp_path))
+    text = _asm(src, tmp_path)
+    # no register spills: these schedules keep every value in registers (a spill would add scratch
+    # memory traffic the schedule does not account for)
+    sizes = re.findall(r"\.amdhsa_private_segment_fixed_size (\d+)", text)
+    assert sizes and all(int(x) == 0 for x in sizes), sizes
+    bodies = _kernel_bodies(text)
     kernels = [(name, code) for name, code in bodies if kernel in name]
     assert len(kernels) == 1, [n for n, _ in bodies]          # d = 128
     for name, code in kernels:
