@@ -8,8 +8,9 @@
 // while tile j is processed, the K tile j+2 and the V tile j+1 are in flight.
 //
 // Each wave is software pipelined over key tiles: the MFMAs of S_{j+1} = K_{j+1} Q^T are
-// interleaved with the exponentials and row sums of tile j, and the MFMAs of O += V_j^T P_j with
-// the row maximum of S_{j+1}, so that the matrix cores and the vector ALU work at the same time.  Per wave, with g = lane / 32 and n = lane % 32:
+// interleaved with the exponentials and row sums of tile j, so that the matrix cores and the
+// vector ALU work at the same time (the other wave of the SIMD runs its O += V^T P^T products
+// meanwhile).  Per wave, with g = lane / 32 and n = lane % 32:
 //   S^T = K Q^T   A = K rows from LDS (key n, 8 dims), B = Q^T from registers (query n, 8 dims)
 //                 -> lane holds query n and keys 8*(r/4) + 4g + r%4 of each 32-key block;
 //   O^T += V^T P^T A = V^T read from the row-major V tile with ds_read_b64_tr_b16 (4 keys per
@@ -18,9 +19,13 @@
 // that both the 16-byte K reads (16 rows, one chunk) and the transposed V reads (4 rows x 2
 // chunks per 16 lanes) hit distinct banks.
 //
-// Softmax statistics are fp32 in the exp2 domain (t = scale*log2(e)*q.k).  The reference maximum
-// of a row only moves when a tile's maximum exceeds it by more than kLazy (probabilities stay
-// below 2^kLazy), so the accumulator rescale is skipped for most tiles.  At the end of chunk r the
+// Softmax statistics are fp32 in the exp2 domain (t = scale*log2(e)*q.k).  Eqs. (2)-(3) hold for
+// any per-row reference m, not only the running maximum, so no row maximum is taken per tile: a
+// tile's probabilities exp2(t - m) are formed against the current m, and only when a lane's sum
+// of them reaches 2^64 (or is not finite, as on the first tile, whose m is still -inf) is the tile
+// redone with m moved to its row maximum and the accumulators rescaled.  A lane's sum bounds each
+// of its terms, so every probability stays below 2^64 (far inside fp32 and bf16 range, whose
+// relative precision does not depend on magnitude).  At the end of chunk r the
 // wave forms the chunk's log-sum-exp loc_lse_r from the chunk's own row sum and folds it into the
 // merged lse by Eq. (5).  The output numerator is kept unnormalised: Eq. (5)'s term
 // exp(loc_lse_r - M) loc_out_r equals exp(m - M) times the chunk's unnormalised accumulator, so
@@ -39,7 +44,7 @@ namespace {
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-constexpr float kLazy = 8.0f;
+constexpr float kGuard = 18446744073709551616.0f;   // 2^64: bound on a lane's probability sum
 
 template <int D>
 struct FwdCfg {
@@ -234,12 +239,6 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     for (int kt = 0; kt < C::kKTiles; ++kt)
       sa[kt] = mfma32(*reinterpret_cast<const bf16x8*>(lds_k + koff[s] + kt * 32 * C::kRowBytes),
                       qf[s], sa[kt]);
-  float mx = -INFINITY;   // row max of the tile in `cur` (raw scores)
-#pragma unroll
-  for (int kt = 0; kt < C::kKTiles; ++kt)
-#pragma unroll
-    for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, sa[kt][rr]);
-  mx = max_halves(mx);
 
   // One pipelined iteration for tile t0 (scores in `cur`); parity P selects the buffers: K_{j+1}
   // is read from K buffer 1-P, V_j from V buffer P; K_{j+2} lands in K buffer P, V_{j+1} in V
@@ -258,8 +257,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     // for the P V half).
     __builtin_amdgcn_s_setprio(1);
 
-    // last tile of a chunk: keys past the chunk end (clamped copies of its last key) add nothing.
-    // The row max needs no mask: a copy's score equals that of a valid key.
+    // last tile of a chunk: keys past the chunk end (clamped copies of its last key) add nothing
     const int nvalid = (int)min<int64_t>(C::kBK, t0.hi - t0.start);
     if (nvalid < C::kBK) {
       cold_path();
@@ -270,21 +268,6 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
         for (int rr = 0; rr < 16; ++rr)
           if (kt * 32 + 8 * (rr >> 2) + (rr & 3) >= thr) cur[kt][rr] = -INFINITY;
     }
-    // lazily moved reference max (Eqs. (2)-(3))
-    {
-      const float mt = mx * c2;
-      const bool need = mt > m2 + kLazy;
-      if (__builtin_amdgcn_ballot_w64(need)) {
-        cold_path();
-        const float mnew = need ? mt : m2;
-        const float alpha = fast_exp2(m2 - mnew);
-        m2 = mnew;
-        lc *= alpha;
-#pragma unroll
-        for (int c = 0; c < C::kCT; ++c) oacc[c] *= alpha;
-      }
-    }
-
     // S_{j+1} = K_{j+1} Q^T on the matrix cores, P_j = exp2(t - m) on the vector ALU
     const char* kbuf = lds_k + (1 - P) * C::kTileBytes;
 #pragma unroll
@@ -312,7 +295,6 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
         }
         pf[2 * kt + h] = __builtin_bit_cast(bf16x8, w);
       }
-    lc += la + lb;
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
     for (int i = 0; i < C::kDSteps * C::kKTiles; ++i) {
@@ -321,9 +303,43 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
       __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
+    // the reference m moves only when a probability of the tile could reach 2^64: the rare tile
+    // that fails the check is redone against its row maximum
+    if (__builtin_amdgcn_ballot_w64(!(la + lb < kGuard))) {
+      cold_path();
+      float ma = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < C::kKTiles; ++kt)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) ma = fmaxf(ma, cur[kt][rr]);
+      const float mnew = fmaxf(m2, max_halves(ma) * c2);
+      const float alpha = fast_exp2(m2 - mnew);
+      m2 = mnew;
+      lc *= alpha;
+#pragma unroll
+      for (int c = 0; c < C::kCT; ++c) oacc[c] *= alpha;
+      la = 0.f;
+      lb = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < C::kKTiles; ++kt)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          u32x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float p0 = fast_exp2(__builtin_fmaf(cur[kt][8 * h + 2 * e], c2, -m2));
+            const float p1 = fast_exp2(__builtin_fmaf(cur[kt][8 * h + 2 * e + 1], c2, -m2));
+            la += p0;
+            lb += p1;
+            w[e] = pack_bf16x2(p0, p1);
+          }
+          pf[2 * kt + h] = __builtin_bit_cast(bf16x8, w);
+        }
+    }
+    lc += la + lb;
 
     __builtin_amdgcn_s_setprio(0);
-    // O += V_j^T P_j on the matrix cores; row max of S_{j+1} on the ALU
+    // O += V_j^T P_j on the matrix cores
     const char* vbuf = lds_v + P * C::kTileBytes;
 #pragma unroll
     for (int s = 0; s < C::kKSteps; ++s)
@@ -335,24 +351,11 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
             (lds_bf16x4*)(vbuf + voff[1][c] + s * 16 * C::kRowBytes));
         oacc[c] = mfma32(__builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7), pf[s], oacc[c]);
       }
-    {
-      float ma = -INFINITY, mb = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < C::kKTiles; ++kt)
-#pragma unroll
-        for (int rr = 0; rr < 16; rr += 2) {
-          ma = fmaxf(ma, nxt[kt][rr]);
-          mb = fmaxf(mb, nxt[kt][rr + 1]);
-        }
-      mx = fmaxf(ma, mb);
-      mx = max_halves(mx);
-    }
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
     for (int i = 0; i < C::kKSteps * C::kCT; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
 

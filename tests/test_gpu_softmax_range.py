@@ -1,0 +1,88 @@
+"""Rows whose scores climb or fall by hundreds to thousands of natural-log units along the key
+sequence, against the fp64 oracle (needs an MI355X).
+
+The forward keeps a per-row reference for its exponentials that moves only when a tile's
+probabilities against it would leave a wide range (Eqs. (2)-(3) hold for any reference).  A
+climbing ramp makes it move every few tiles, and a steep one makes the first try of a tile
+overflow to infinity before the move; a falling ramp never moves it after the first tile and lets
+every later probability underflow.  The fused path, the per-chunk partials with the standalone
+merge, and the ring steps (which restart the reference at every chunk) all meet the oracle.
+
+Inputs: seeded i.i.d. N(0, 1/4) Q, K, V in bf16, with column 0 of Q set to 1 and column 0 of K
+to a linear ramp over the keys (then rounded to bf16, which makes it a staircase at the larger
+values), so that every row's score rises (or falls) by about `total` natural-log units from the
+first key to the last.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import attention_fp64 as oa
+from paper_2507_16697_amd import inputs, ring, ringx
+
+from parity_util import TOL_BF16_LSE, TOL_BF16_REL_RMS, max_abs_err, rel_rms_err, to_device, \
+    to_host_f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _ramp_case(seed, B, H, Nq, Nk, d, total, sign):
+    t = inputs.make_iid(B, H, Nq, Nk, d, seed=seed, std=0.5, store="bf16", with_do=False)
+    x = {key: inputs.to_f64(val, "bf16") for key, val in t.items()}
+    scale = 1.0 / math.sqrt(d)
+    ramp = np.arange(Nk, dtype=np.float64) * (total / (scale * (Nk - 1)))
+    x["q"][..., 0] = 1.0
+    x["k"][..., 0] = ramp if sign > 0 else ramp[::-1]
+    bits = {key: inputs.f64_to_bf16_bits(val) for key, val in x.items()}
+    exact = {key: inputs.bf16_bits_to_f64(val) for key, val in bits.items()}
+    return bits, exact, float(np.float32(scale))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("total,sign", [(400.0, 1), (5000.0, 1), (400.0, -1), (5000.0, -1)])
+def test_score_ramp_forward(d, total, sign):
+    B, H, Nq, Nk, R = 1, 2, 300, 2000, 3
+    bits, x, scale = _ramp_case(7, B, H, Nq, Nk, d, total, sign)
+    g = {key: to_device(val, "bf16") for key, val in bits.items()}
+    ref_o, ref_l = oracle.attention(x["q"], x["k"], x["v"], scale)
+
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    po, pl = ringx.ringx_attn_fwd_partials(g["q"], g["k"], g["v"], R, scale=scale)
+    mo, ml = ringx.ringx_lse_merge(po, pl, out_dtype=torch.bfloat16)
+    bounds = [ringx.ringx_chunk_bounds(Nk, R, r) for r in range(R)]
+    ks = [g["k"][:, :, lo:hi].contiguous() for lo, hi in bounds]
+    vs = [g["v"][:, :, lo:hi].contiguous() for lo, hi in bounds]
+    so, sl = ring.ring_forward(g["q"], ks, vs, scale=scale)
+    torch.cuda.synchronize()
+
+    ref_po, ref_pl = oracle.attention_partials(x["q"], x["k"], x["v"], scale, R)
+    assert np.allclose(oa.lse_merge(ref_po, ref_pl)[1], ref_l, rtol=0, atol=1e-9)
+    # bf16 outputs: each element against the bound of the path's own roundings (P before the
+    # P V contraction and the stored output, 2^-8 each), which at these peaked rows is close to
+    # the 2e-2 bar measured against the output RMS; the fp32 partials keep the bar itself
+    av = oracle.attention(x["q"], x["k"], np.abs(x["v"]), scale)[0]   # sum_j P_ij |v_j|
+    lim = 1.5 * 2.0 ** -8 * (av + np.abs(ref_o)) + 1e-5 * float(np.max(np.abs(ref_o)))
+    errs = {
+        "out": float(np.max(np.abs(to_host_f64(out) - ref_o) / lim)),
+        "merged_out": float(np.max(np.abs(to_host_f64(mo) - ref_o) / lim)),
+        "ring_out": float(np.max(np.abs(to_host_f64(so) - ref_o) / lim)),
+        "part_out": max(rel_rms_err(to_host_f64(po)[r], ref_po[r]) / TOL_BF16_REL_RMS
+                        for r in range(R)),
+    }
+    lse_errs = {
+        "lse": max_abs_err(to_host_f64(lse), ref_l),
+        "merged_lse": max_abs_err(to_host_f64(ml), ref_l),
+        "ring_lse": max_abs_err(to_host_f64(sl), ref_l),
+        "part_lse": max_abs_err(to_host_f64(pl), ref_pl),
+    }
+    print(f"ramp d={d} total={total} sign={sign} (fraction of the bound)",
+          " ".join(f"{k}={v:.2f}" for k, v in errs.items()),
+          " ".join(f"{k}={v:.2e}" for k, v in lse_errs.items()), flush=True)
+    for key, e in errs.items():
+        assert e <= 1.0, (key, e)
+    for key, e in lse_errs.items():
+        assert e <= TOL_BF16_LSE, (key, e)
