@@ -9,9 +9,11 @@
 // atomics (the paper's "gradient for Q accumulated over N steps").  Per 32-key block ("unit") and
 // query block, with lane = query n and g = lane / 32:
 //   S^T  = K Q^T      A = K rows (LDS),  B = Q^T from registers
-//   dP^T = V dO^T     A = V rows (LDS),  B = dO^T from registers
+//   dP^T - D = V dO^T - D   A = V rows (LDS), B = dO^T from registers, accumulators start at -D
 //   P^T  = exp2(S^T * scale*log2e - lse_q*log2e),  dS^T = P^T (dP^T - D_q)   (lse_q, D_q are
-//          per-lane scalars because each lane holds one query)
+//          per-lane scalars because each lane holds one query; -D_q fills a 16-register block
+//          per query block that starts every dP^T chain, so the subtraction rides on the
+//          matrix cores)
 //   dQ^T += K^T dS^T  A = K^T by transposed reads of the row-major K tile, B = dS^T from the
 //          registers (keys 4g..4g+3, 8+4g..8+4g+3 of each 16-key step, as in the forward)
 // Every LDS operand feeds the products of both query blocks, so a wave reads half a KiB of LDS per
@@ -182,11 +184,20 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     nl[b] = -lse[bh * Nq + qi] * kLog2e;
     dd[b] = delta[bh * Nq + qi];
   }
-  // the fragments are in AGPRs, two wait states before the first product that reads them
+  // -D of each query block as the start of its dP^T chains (the lane's query is the same for all
+  // 16 accumulators), so that the products return dP - D
+  f32x16 negd[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) negd[b][e] = -dd[b];
+  // the fragments are in AGPRs and -D in VGPRs, two wait states before the first product that
+  // reads them
 #pragma unroll
   for (int b = 0; b < 2; ++b)
 #pragma unroll
     for (int s = 0; s < C::kDSteps; ++s) asm volatile("" : "+a"(qf[b][s]), "+a"(of[b][s]));
+  asm volatile("" : "+v"(negd[0]), "+v"(negd[1]));
   asm volatile("s_nop 2");
 
   // per-lane LDS offsets: K/V rows (A operands of S^T, dP^T) and transposed K (A of dQ^T)
@@ -254,10 +265,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     const int grp_i = k >> 3, e8 = k & 7;
     const int b = grp_i & 1, ks = grp_i >> 1;
     const int e = 8 * ks + e8;
-    float se = sc[b][e], de = dp[b][e];
+    float se = sc[b][e], de = dp[b][e];   // de = dP - D
     asm volatile("" : "+v"(se), "+v"(de));
     const float pe = fast_exp2(__builtin_fmaf(se, c2, nl[b]));
-    dse[b][e] = pe * (de - dd[b]);
+    dse[b][e] = pe * de;
     if (e8 & 1) {
       uint32_t a2 = pack_bf16x2(dse[b][e - 1], dse[b][e]);
       asm volatile("" : "+v"(a2));
@@ -281,7 +292,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
       const bool is_dp = (i & 2) != 0;
       f32x16& acc = is_dp ? ndp[b] : nsc[b];
       const bf16x8 bop = is_dp ? of[b][s] : qf[b][s];
-      if (s == 0) mfma_first_v(acc, abuf[i >> 1], bop);
+      if (s == 0 && is_dp) mfma_first_vc(acc, abuf[i >> 1], bop, negd[b]);
+      else if (s == 0) mfma_first_v(acc, abuf[i >> 1], bop);
       else mfma_acc_v(acc, abuf[i >> 1], bop);
 #pragma unroll
       for (int e = (i * kE) / kM1; e < ((i + 1) * kE) / kM1; ++e) elem(sc, dp, 8 + e, sw);
@@ -330,7 +342,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     f32x16& acc = is_dp ? pa[b] : sa[b];
     const bf16x8 aop = read_a(i, 0, 0);
     const bf16x8 bop = is_dp ? of[b][s] : qf[b][s];
-    if (s == 0) mfma_first_v(acc, aop, bop);
+    if (s == 0 && is_dp) mfma_first_vc(acc, aop, bop, negd[b]);
+    else if (s == 0) mfma_first_v(acc, aop, bop);
     else mfma_acc_v(acc, aop, bop);
   }
   asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sa[0]), "+v"(sa[1]), "+v"(pa[0]), "+v"(pa[1]));
