@@ -98,6 +98,116 @@ def _cpu_model():
     return "unknown"
 
 
+def _time(torch, stream, fn, warmup, n):
+    """Per-call milliseconds of fn (HIP events on `stream`): sorted list of n values."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return sorted(a.elapsed_time(b) for a, b in ev)
+
+
+def _stats(ms, flops):
+    med = ms[len(ms) // 2]
+    return {"ms_min": ms[0], "ms_median": med, "ms_max": ms[-1], "calls": len(ms),
+            "tflops_median": flops / (med * 1e-3) / 1e12,
+            "frac_median": flops / (med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+
+
+def other_shapes(torch, np, inputs, ringx, stream, dev):
+    """Timings of the other paper-shaped workloads: the 16k single shard (fwd+bwd, d=64), the
+    turbulence tokens (fwd, d=64, inputs from the host recipe: 256^3 field, 4^3 patches, seeded
+    embedding and projections) and the 524k long step (fwd+bwd, d=128, plus the standalone merge).
+    The i.i.d. workloads are drawn on the device (torch's seeded generator, the workload's
+    distribution) so that the run stays short; their parity tests use the host recipe."""
+    res = {}
+    gen = torch.Generator(device=dev)
+
+    def iid(w, seed):
+        gen.manual_seed(seed)
+        bf = dict(dtype=torch.bfloat16, device=dev)
+        x = {n: (torch.randn((w.B, w.H, N, w.d), generator=gen, device=dev) * w.std).to(**bf)
+             for n, N in (("q", w.Nq), ("k", w.Nk), ("v", w.Nk))}
+        x["do"] = (torch.randn((w.B, w.H, w.Nq, w.d), generator=gen, device=dev)
+                   * w.do_std).to(**bf)
+        return x
+
+    def fwd_bwd(w, x, warmup, n):
+        q, k, v, do = x["q"], x["k"], x["v"], x["do"]
+        B, H, Nq, Nk, d, R = w.B, w.H, w.Nq, w.Nk, w.d, w.R
+        out = torch.empty_like(q)
+        lse = torch.empty((B, H, Nq), dtype=torch.float32, device=dev)
+        delta = torch.empty_like(lse)
+        dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=dev)
+        dk = torch.empty((B, H, Nk, d), dtype=torch.float32, device=dev)
+        dv = torch.empty_like(dk)
+
+        def step():
+            ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
+            ringx.ringx_bwd_preprocess(out, do, delta=delta, stream=stream)
+            ringx.ringx_attn_bwd_dkdv(q, k, v, do, lse, delta, R, scale=w.scale, dk=dk, dv=dv,
+                                      stream=stream)
+            ringx.ringx_attn_bwd_dq(q, k, v, do, lse, delta, R, scale=w.scale, dq=dq,
+                                    stream=stream)
+
+        r = _stats(_time(torch, stream, step, warmup, n), 6 * w.gemm_unit())
+        r.update(workload=w.name, B=B, H=H, Nq=Nq, Nk=Nk, d=d, R=R, passes="fwd+bwd",
+                 flops=6 * w.gemm_unit(), inputs="device-drawn i.i.d., the workload's distribution")
+        if not bool(torch.isfinite(dq).all()):
+            raise RuntimeError(f"non-finite results at {w.name}")
+        return r
+
+    w = inputs.WORKLOADS["shard_n16k_d64"]
+    res[w.name] = fwd_bwd(w, iid(w, w.seed), 3, 10)
+    log(f"[bench] {w.name}: {res[w.name]['ms_median']:.2f} ms/step, "
+        f"{res[w.name]['tflops_median']:.1f} TFLOP/s")
+
+    w = inputs.WORKLOADS["turbulence_nk262k_d64"]
+    t0 = time.time()
+    tt = inputs.make_workload(w.name)
+    log(f"[bench] {w.name} inputs (host recipe) in {time.time() - t0:.1f}s")
+    q, k, v = (torch.from_numpy(np.ascontiguousarray(tt[n]).view(np.int16)).to(dev)
+               .view(torch.bfloat16) for n in ("q", "k", "v"))
+    del tt
+    out = torch.empty_like(q)
+    lse = torch.empty((w.B, w.H, w.Nq), dtype=torch.float32, device=dev)
+    ms = _time(torch, stream, lambda: ringx.ringx_attn_fwd(q, k, v, w.R, scale=w.scale, out=out,
+                                                           lse=lse, stream=stream), 1, 5)
+    res[w.name] = _stats(ms, 2 * w.gemm_unit())
+    res[w.name].update(workload=w.name, B=w.B, H=w.H, Nq=w.Nq, Nk=w.Nk, d=w.d, R=w.R,
+                       passes="fwd", flops=2 * w.gemm_unit(), inputs="host recipe")
+    log(f"[bench] {w.name}: {res[w.name]['ms_median']:.2f} ms/fwd, "
+        f"{res[w.name]['tflops_median']:.1f} TFLOP/s")
+    del q, k, v, out, lse
+
+    w = inputs.WORKLOADS["long_nk524k_d128"]
+    x = iid(w, w.seed)
+    res[w.name] = fwd_bwd(w, x, 1, 5)
+    log(f"[bench] {w.name}: {res[w.name]['ms_median']:.1f} ms/step, "
+        f"{res[w.name]['tflops_median']:.1f} TFLOP/s")
+    po, pl = ringx.ringx_attn_fwd_partials(x["q"], x["k"], x["v"], w.R, scale=w.scale,
+                                           stream=stream)
+    mo = torch.empty_like(x["q"])
+    ml = torch.empty((w.B, w.H, w.Nq), dtype=torch.float32, device=dev)
+    ms = _time(torch, stream, lambda: ringx.ringx_lse_merge(po, pl, out=mo, lse=ml, stream=stream),
+               2, 10)
+    rows = w.B * w.H * w.Nq
+    mbytes = w.R * rows * (4 * w.d + 4) + rows * (2 * w.d + 4)
+    med = ms[len(ms) // 2]
+    res[w.name]["lse_merge"] = {"ms_median": med, "bytes": mbytes,
+                                "GB/s": mbytes / (med * 1e-3) / 1e9,
+                                "frac": mbytes / (med * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    log(f"[bench] {w.name} lse_merge {med:.3f} ms, {mbytes / (med * 1e-3) / 1e9:.0f} GB/s")
+    del x, po, pl, mo, ml
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +223,9 @@ def main():
                     help="skip the grouped-query measurement (H/4 K/V heads)")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the ring-step measurement (chunks arriving on a second stream)")
+    ap.add_argument("--no-shapes", action="store_true",
+                    help="skip the other paper-shaped workloads (16k single shard, turbulence "
+                         "tokens, 524k long step)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -202,6 +315,7 @@ def main():
     fwd_ms, pre_ms, dkdv_ms, dq_ms = avg(0, 1), avg(1, 2), avg(2, 3), avg(3, 4)
     bwd_ms = pre_ms + dkdv_ms + dq_ms
     ms_step = total_ms / K
+    per_step = sorted(e[0].elapsed_time(e[4]) for e in ev)
     log(f"[bench] timed {K} steps: {ms_step:.2f} ms/step (fwd {fwd_ms:.2f}, bwd {bwd_ms:.2f} = "
         f"pre {pre_ms:.3f} + dkdv {dkdv_ms:.2f} + dq {dq_ms:.2f}; wall {wall * 1e3 / K:.2f})")
     if not (torch.isfinite(out.float()).all() and torch.isfinite(dq).all()):
@@ -359,6 +473,11 @@ def main():
                                               for m in modes))
         del field
 
+    # the other paper-shaped workloads (parity-test cases, reported beside the headline)
+    if not args.no_shapes:
+        del out, dq, dk, dv
+        kernels["other_shapes"] = other_shapes(torch, np, inputs, ringx, stream, dev)
+
     result = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
@@ -367,11 +486,14 @@ def main():
                    "flops_per_step": 6 * U, "flop_convention": "12*B*H*Nq*Nk*d per fwd+bwd step",
                    "fwd_ms": fwd_ms, "bwd_ms": bwd_ms, "bwd_pre_ms": pre_ms,
                    "bwd_dkdv_ms": dkdv_ms, "bwd_dq_ms": dq_ms,
+                   "step_ms_min": per_step[0], "step_ms_median": per_step[len(per_step) // 2],
+                   "step_ms_max": per_step[-1],
                    "tflops_fa_convention_14": 7 * U / (ms_step * 1e-3) / 1e12},
         "pct_of_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "roofline": roofline,
         "kernels": kernels,
         "gpu": torch.cuda.get_device_name(0),
+        "hip": torch.version.hip,
     }
     if not args.no_cpu_baseline:
         log(f"[bench] cpu baseline: oracle on {args.cpu_rows} query rows of head 0")
