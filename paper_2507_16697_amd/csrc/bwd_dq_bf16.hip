@@ -23,9 +23,9 @@
 // unit u issues the 32 S/dP products of unit u+1, beside the P/dS arithmetic of three of the four
 // 8-element groups of unit u; phase 2 issues the 16 dQ products of unit u, beside the first group
 // of unit u+1 (started a few products late, so that the S/dP products just issued have
-// finished).  A product slot carries at most one element (fma, exp, subtract, multiply, half a
-// pack): one hides behind the 32-cycle product, two do not.  LDS operands are read 8 products
-// ahead.  Key rows past the end of a chunk (last tile of a chunk) are clamped copies, zeroed in the
+// finished).  A product slot carries at most one element (fma, exp, multiply, half a pack; the
+// subtraction of D rides on the products): one hides behind the 32-cycle product, two do not.
+// LDS operands are read 10 products ahead.  Key rows past the end of a chunk (last tile of a chunk) are clamped copies, zeroed in the
 // K stage once they land: their dS then meets a zero K^T row and adds nothing, so the loop has no
 // masking.
 //
@@ -234,7 +234,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
 
   constexpr int kM1 = 4 * C::kDSteps;   // S and dP products of one unit, both query blocks
   constexpr int kM2 = 4 * C::kCT;       // dQ products of one unit, both query blocks
-  constexpr int kPf = 8;                // operand reads run this many products ahead
+  constexpr int kPf = 10;               // operand reads run this many products ahead
   constexpr int kLate = 4;              // phase 2 starts its arithmetic this many products late
   static_assert(kM1 >= kPf && kM2 >= kPf && kM2 - kLate >= 8, "pipeline shape");
 
