@@ -50,6 +50,27 @@ def _bf16_err(got, ref):
 
 @pytest.mark.parametrize("case", _cases(), ids=lambda c: "-".join(str(x) for x in c))
 def test_sweep(case):
+    _run_case(case)
+
+
+# Shapes with a handful of queries or keys, from a wider one-off sweep (150 shapes of another
+# seed): their bf16 gradients stay within a tenth of the element-wise rounding bound, but with so
+# few rows a gradient's RMS is small against the bf16 rounding of its largest terms (and of D,
+# formed from the bf16 output), and the max-abs / RMS measure reaches 2.4e-2.  They are held to
+# the bound; the output and lse keep the RMS and lse bars.
+DEGENERATE = [(3005, "bf16", 2, 2, 1, 21, 483, 128, 2),     # 21 queries: dK
+              (3137, "bf16", 1, 1, 1, 500, 3, 128, 3),      # 3 keys in 3 chunks: dQ
+              (3200, "bf16", 1, 2, 2, 7, 1099, 64, 13),
+              (3201, "bf16", 2, 1, 4, 1, 64, 128, 64),
+              (3202, "bf16", 1, 1, 1, 300, 1, 64, 1)]
+
+
+@pytest.mark.parametrize("case", DEGENERATE, ids=lambda c: "-".join(str(x) for x in c))
+def test_degenerate_shapes_within_rounding_bound(case):
+    _run_case(case, grads_rms=False)
+
+
+def _run_case(case, grads_rms=True):
     i, store, B, hkv, grp, nq, nk, d, R = case
     H = hkv * grp
     std, do_std = ((0.5, 1.0) if d == 64 else (2 ** -0.5, 2 ** -0.5)) if store == "bf16" \
@@ -98,7 +119,7 @@ def test_sweep(case):
             errs[key] = (e, TOL_F32)
         elif key.endswith("lse"):
             errs[key] = (max_abs_err(got[key], ref[key]), TOL_BF16_LSE)
-        else:
+        elif grads_rms or key not in ("dq", "dk", "dv"):
             errs[key] = (_bf16_err(got[key], ref[key]), TOL_BF16_REL_RMS)
     if store == "bf16":
         # every element also within 1.5x the bound of the path's roundings
