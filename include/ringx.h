@@ -34,7 +34,10 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#if defined(__HIPCC__) || defined(__HIP_PLATFORM_AMD__)
+/* hipStream_t: from the HIP runtime when hipcc compiles the includer; otherwise the same opaque
+   handle type, so that plain C and C++ callers need no HIP headers (a repeated identical typedef
+   is valid in C11 and C++). */
+#ifdef __HIPCC__
 #include <hip/hip_runtime_api.h>
 #else
 typedef struct ihipStream_t* hipStream_t;
