@@ -22,10 +22,11 @@
 // Softmax statistics are fp32 in the exp2 domain (t = scale*log2(e)*q.k).  Eqs. (2)-(3) hold for
 // any per-row reference m, not only the running maximum, so no row maximum is taken per tile: a
 // tile's probabilities exp2(t - m) are formed against the current m, and only when a lane's sum
-// of them reaches 2^64 (or is not finite, as on the first tile, whose m is still -inf) is the tile
+// of them reaches 2^32 (or is not finite, as on the first tile, whose m is still -inf) is the tile
 // redone with m moved to its row maximum and the accumulators rescaled.  A lane's sum bounds each
-// of its terms, so every probability stays below 2^64 (far inside fp32 and bf16 range, whose
-// relative precision does not depend on magnitude).  At the end of chunk r the
+// of its terms, so every probability stays below 2^32: bf16 and fp32 keep the same relative
+// precision at any magnitude, and a row sum or output accumulator of at most 2^32 per key stays
+// far inside the fp32 range for any realistic V.  At the end of chunk r the
 // wave forms the chunk's log-sum-exp loc_lse_r from the chunk's own row sum and folds it into the
 // merged lse by Eq. (5).  The output numerator is kept unnormalised: Eq. (5)'s term
 // exp(loc_lse_r - M) loc_out_r equals exp(m - M) times the chunk's unnormalised accumulator, so
@@ -44,7 +45,7 @@ namespace {
 
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
-constexpr float kGuard = 18446744073709551616.0f;   // 2^64: bound on a lane's probability sum
+constexpr float kGuard = 4294967296.0f;   // 2^32: bound on a lane's probability sum
 
 template <int D>
 struct FwdCfg {
@@ -308,7 +309,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
       __builtin_amdgcn_sched_group_barrier(0x002, kValuPerProduct, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // the reference m moves only when a probability of the tile could reach 2^64: the rare tile
+    // the reference m moves only when a probability of the tile could reach 2^32: the rare tile
     // that fails the check is redone against its row maximum
     if (__builtin_amdgcn_ballot_w64(!(la + lb < kGuard))) {
       cold_path();
