@@ -25,9 +25,10 @@
 // of unit u+1 (started a few products late, so that the S/dP products just issued have
 // finished).  A product slot carries at most one element (fma, exp, multiply, half a pack; the
 // subtraction of D rides on the products): one hides behind the 32-cycle product, two do not.
-// LDS operands are read 10 products ahead.  Key rows past the end of a chunk (last tile of a chunk) are clamped copies, zeroed in the
-// K stage once they land: their dS then meets a zero K^T row and adds nothing, so the loop has no
-// masking.
+// LDS operands are read 10 products ahead.  Key rows past the end of a chunk (last tile of a
+// chunk) are clamped copies of its last key; in the units that hold them (a branch outside the
+// product schedule, between the phases) their scores are set to -inf once the S^T products have
+// finished, so P and dS are exactly 0 there whatever the row's lse.
 //
 // Register files: Q/dO fragments (128) and the dQ^T accumulators (128) in AGPRs, the S/dP
 // accumulators of two units, dS^T and the operands in flight in VGPRs; the products are the
@@ -99,7 +100,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
   const char* vb = reinterpret_cast<const char*>(v + kvh * Nk * D);
 
   // Tiles: chunk r covers keys [r Nk / R, (r+1) Nk / R), cut into 64-key tiles from its start.
-  // ld_*: the next tile to load; nx_*: the tile after the one being computed (zeroed on landing).
+  // ld_*: the next tile to load; nx_*: the tile after the one being computed.
   int64_t ld_start = 0, ld_hi = Nk / R;
   int ld_r = 0;
   int64_t nx_start = 0, nx_hi = Nk / R;
@@ -150,13 +151,6 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
       }
     }
     advance(ld_start, ld_hi, ld_r);
-  };
-  // K rows valid .. 63 of the tile in `stage` to zero (called between barriers once it landed)
-  auto zero_k = [&](int stage, int valid) {
-    char* kt = lds + stage * C::kStage;
-    for (int i = t; i < (C::kBK - valid) * C::kChunks; i += C::kThreads)
-      *reinterpret_cast<u32x4*>(kt + (valid + i / C::kChunks) * C::kRowBytes +
-                                (i % C::kChunks) * 16) = u32x4{};
   };
 
 #pragma unroll
@@ -224,13 +218,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
 #pragma unroll
     for (int c = 0; c < C::kCT; ++c) dqacc[b][c] = f32x16{};
 
+  // keys of the tile being computed (cur_valid) and of the next one (nx_valid) that lie inside
+  // their chunk: 64 except in the last tile of a chunk
+  int cur_valid = (int)min<int64_t>(C::kBK, nx_hi - nx_start);
+  int nx_valid = C::kBK;
+
   wait_vmem<0>();
   __syncthreads();
-  if (ntiles > 0 && nx_start + C::kBK > nx_hi) {
-    cold_path();
-    zero_k(0, (int)(nx_hi - nx_start));
-    __syncthreads();
-  }
 
   constexpr int kM1 = 4 * C::kDSteps;   // S and dP products of one unit, both query blocks
   constexpr int kM2 = 4 * C::kCT;       // dQ products of one unit, both query blocks
@@ -324,6 +318,19 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     }
   };
 
+  // Scores of key rows nvalid .. 31 of a unit (S^T rows 8 (e / 4) + 4 g + e % 4) to -inf, so
+  // that P = 0 and dS = 0 for keys past the end of a chunk.  Cold: only the last tile of a chunk
+  // whose length is not a multiple of 64 gets here.  The wait lets the S^T products finish.
+  auto mask_rows = [&](f32x16 (&sc)[2], int nvalid) {
+    cold_path();
+    asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sc[0]), "+v"(sc[1]));
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (8 * (e >> 2) + 4 * g + (e & 3) >= nvalid) sc[b][e] = -INFINITY;
+  };
+
   // Unit 0 of every tile lives in (sa, pa, swa), unit 1 in (sb, pb, swb).
   f32x16 sa[2], pa[2], sb[2], pb[2];
   u32x4 swa[2][2], swb[2][2];
@@ -347,6 +354,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     else mfma_acc_v(acc, aop, bop);
   }
   asm volatile("s_nop 15\n\ts_nop 15" : "+v"(sa[0]), "+v"(sa[1]), "+v"(pa[0]), "+v"(pa[1]));
+  if (cur_valid < 32) mask_rows(sa, cur_valid);
 #pragma unroll
   for (int e = 0; e < 8; ++e) elem(sa, pa, e, swa);
 #pragma unroll
@@ -361,11 +369,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     else wait_vmem<0>();
     __syncthreads();
     advance(nx_start, nx_hi, nx_r);
-    if (it + 1 < ntiles && nx_start + C::kBK > nx_hi) {
-      cold_path();
-      zero_k((it + 1) & 3, (int)(nx_hi - nx_start));
-      __syncthreads();
-    }
+    if (it + 1 < ntiles) nx_valid = (int)min<int64_t>(C::kBK, nx_hi - nx_start);
     if (it + 3 < ntiles) issue_next((it + 3) & 3);
     __builtin_amdgcn_sched_barrier(0);
 
@@ -373,11 +377,14 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     // unit 0 of tile it (next: unit 1 of tile it; then unit 0 of tile it+1, a stale stage after
     // the last tile, whose results are not used)
     phase1(sa, pa, sb, pb, swa, st_cur, 0, st_cur, 1);
+    if (cur_valid < C::kBK) mask_rows(sb, cur_valid - 32);
     as_bf16(swa, sf);
     phase2(sf, sb, pb, swb, st_cur, 0, st_nxt, 0);
     phase1(sb, pb, sa, pa, swb, st_cur, 1, st_nxt, 0);
+    if (nx_valid < 32) mask_rows(sa, nx_valid);
     as_bf16(swb, sf);
     phase2(sf, sa, pa, swa, st_cur, 1, st_nxt, 1);
+    cur_valid = nx_valid;
     // after the last products, before any code at the loop exit reads or moves the accumulators
     if (it + 1 == ntiles) asm volatile("s_nop 15\n\ts_nop 15");
   }

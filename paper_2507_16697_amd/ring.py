@@ -47,7 +47,21 @@ class _PingPong:
             self.view("k", slot, n).copy_(k, non_blocking=True)
             self.view("v", slot, n).copy_(v, non_blocking=True)
             self.ready[slot].record(copy_stream)
+        # the sources are read on the copy stream: keep their memory from being reused before
+        k.record_stream(copy_stream)
+        v.record_stream(copy_stream)
         self.used[slot] = True
+
+
+def _start(torch, compute, overlap, like, nmax):
+    """The copy stream and the ping-pong buffers.  The copy stream first waits for everything
+    enqueued on the compute stream so far: the chunks may have been produced there just before the
+    call, and the buffers' memory may have been freed by work still running there."""
+    copy = torch.cuda.Stream() if overlap else compute
+    pp = _PingPong(torch, like, nmax, copy)
+    if overlap:
+        copy.wait_stream(compute)
+    return copy, pp
 
 
 def _check_chunks(q, k_chunks, v_chunks):
@@ -68,8 +82,7 @@ def ring_forward(q, k_chunks, v_chunks, scale=None, out_dtype=None, overlap=True
     _check_chunks(q, k_chunks, v_chunks)
     B, H, Nq, d = q.shape
     compute = torch.cuda.current_stream()
-    copy = torch.cuda.Stream() if overlap else compute
-    pp = _PingPong(torch, k_chunks[0], max(k.shape[2] for k in k_chunks), copy)
+    copy, pp = _start(torch, compute, overlap, k_chunks[0], max(k.shape[2] for k in k_chunks))
     out_acc = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
     lse_acc = torch.empty((B, H, Nq), dtype=torch.float32, device=q.device)
     pp.fill(torch, copy, 0, k_chunks[0], v_chunks[0])
@@ -95,8 +108,7 @@ def ring_backward(q, k_chunks, v_chunks, out, dout, lse, scale=None, overlap=Tru
     _check_chunks(q, k_chunks, v_chunks)
     B, H, Nq, d = q.shape
     compute = torch.cuda.current_stream()
-    copy = torch.cuda.Stream() if overlap else compute
-    pp = _PingPong(torch, k_chunks[0], max(k.shape[2] for k in k_chunks), copy)
+    copy, pp = _start(torch, compute, overlap, k_chunks[0], max(k.shape[2] for k in k_chunks))
     delta = ringx.ringx_bwd_preprocess(out, dout, stream=compute)
     dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
     dks = [torch.empty(k.shape, dtype=torch.float32, device=q.device) for k in k_chunks]

@@ -146,6 +146,42 @@ def test_ring_overlap_does_not_change_results():
     assert all(torch.equal(x, y) for x, y in zip(a[1] + a[2], b[1] + b[2]))
 
 
+def test_ring_chunks_produced_just_before_the_call():
+    """Chunks written by kernels on the current stream right before ring_forward/ring_backward
+    (behind a long queue of other work there): the copy stream must wait for them, so the results
+    equal those of chunks that were ready long before."""
+    B, H, Nq, Nk, d = 1, 2, 150, 640, 128
+    t, _ = random_case(48, B, H, Nq, Nk, d, store="bf16", std=2 ** -0.5)
+    g = {k: to_device(v, "bf16") for k, v in t.items()}
+    bounds = _even_bounds(Nk, 4)
+    ref_ks, ref_vs = _chunks(g["k"], bounds), _chunks(g["v"], bounds)
+    o_ref, l_ref = ring.ring_forward(g["q"], ref_ks, ref_vs)
+    b_ref = ring.ring_backward(g["q"], ref_ks, ref_vs, o_ref, g["do"], l_ref)
+    torch.cuda.synchronize()
+
+    def busy():
+        # a few milliseconds of fp32 work queued on the current stream
+        x = torch.rand(4096, 4096, device="cuda")
+        for _ in range(8):
+            x = torch.sin(x @ x) * 0.01
+        return x
+
+    def produce(chunks):
+        # each chunk comes out of an elementwise kernel on the current stream
+        return [(c.float() * 1.0).to(torch.bfloat16) for c in chunks]
+
+    busy()
+    ks, vs = produce(ref_ks), produce(ref_vs)
+    o, l = ring.ring_forward(g["q"], ks, vs)
+    busy()
+    ks2, vs2 = produce(ref_ks), produce(ref_vs)
+    b = ring.ring_backward(g["q"], ks2, vs2, o_ref, g["do"], l_ref)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o_ref) and torch.equal(l, l_ref)
+    assert torch.equal(b[0], b_ref[0])
+    assert all(torch.equal(x, y) for x, y in zip(b[1] + b[2], b_ref[1] + b_ref[2]))
+
+
 @pytest.mark.slow
 def test_ring_steps_at_full_size():
     """The 8-way ring share (Nq=32768, Nk=262144 as 8 chunks of 32768) run step by step: the

@@ -24,8 +24,8 @@ import oracle
 from oracle import attention_fp64 as oa
 from paper_2507_16697_amd import inputs, ring, ringx
 
-from parity_util import TOL_BF16_LSE, TOL_BF16_REL_RMS, max_abs_err, rel_rms_err, to_device, \
-    to_host_f64
+from parity_util import TOL_BF16_LSE, TOL_BF16_REL_RMS, max_abs_err, rel_rms_err, \
+    rounding_bounds, to_device, to_host_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -86,3 +86,69 @@ def test_score_ramp_forward(d, total, sign):
         assert e <= 1.0, (key, e)
     for key, e in lse_errs.items():
         assert e <= TOL_BF16_LSE, (key, e)
+
+
+def _shifted_case(seed, B, H, Nq, Nk, d, shift):
+    """Seeded inputs whose every score is moved by about `shift` natural-log units: column 0 of K
+    set to 1 and column 0 of Q to one constant c with scale * c close to shift (c a bf16 value),
+    so that every row's lse lies near shift + log(Nk) and the softmax itself is unchanged."""
+    std, do_std = (0.5, 1.0) if d == 64 else (2 ** -0.5, 2 ** -0.5)
+    t = inputs.make_iid(B, H, Nq, Nk, d, seed=seed, std=std, store="bf16", do_std=do_std)
+    x = {key: inputs.to_f64(val, "bf16") for key, val in t.items()}
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    x["q"][..., 0] = shift / scale
+    x["k"][..., 0] = 1.0
+    bits = {key: inputs.f64_to_bf16_bits(val) for key, val in x.items()}
+    exact = {key: inputs.bf16_bits_to_f64(val) for key, val in bits.items()}
+    return bits, exact, scale
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("shift", [-200.0, 200.0])
+def test_shifted_scores_backward(d, shift):
+    """Every row's lse near -193 (or +207), chunks whose lengths are not multiples of the key
+    tiles (1000 keys in 3 chunks, 300 queries): the fused backward and the ring-step backward
+    against the oracle.  With lse below about -88, a padded key slot whose score were 0 would
+    give exp(-lse) = inf; the kernels mask those slots, so every gradient stays finite.
+
+    A constant column this large makes some gradient sums cancel: dK's column 0 is c times
+    sum_i dS_ij, and D (formed from the bf16 output) is exact only up to its rounding, so the
+    max-abs / RMS measure of dK grows with c although every element stays within the rounding
+    bound of the path (P and dS rounded to bf16, the output stored in bf16, D formed from it).
+    The gradients are held to that bound element by element (1.5x margin), out, dV and lse to
+    the usual bars."""
+    B, H, Nq, Nk, R = 1, 2, 300, 1000, 3
+    bits, x, scale = _shifted_case(11, B, H, Nq, Nk, d, shift)
+    g = {key: to_device(val, "bf16") for key, val in bits.items()}
+    out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
+    dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
+    bounds = [ringx.ringx_chunk_bounds(Nk, R, r) for r in range(R)]
+    ks = [g["k"][:, :, lo:hi].contiguous() for lo, hi in bounds]
+    vs = [g["v"][:, :, lo:hi].contiguous() for lo, hi in bounds]
+    rq, rks, rvs = ring.ring_backward(g["q"], ks, vs, out, g["do"], lse, scale=scale)
+    torch.cuda.synchronize()
+
+    ref_o, ref_l = oracle.attention(x["q"], x["k"], x["v"], scale)
+    oq, ok, ov = oracle.attention_bwd(x["q"], x["k"], x["v"], ref_o, x["do"], ref_l, scale)
+    _, b_dq, b_dk, b_dv = rounding_bounds(x, x["k"], x["v"], ref_o, ref_l, scale)
+    got = {"dq": dq, "dk": dk, "dv": dv, "ring_dq": rq, "ring_dk": torch.cat(rks, dim=2),
+           "ring_dv": torch.cat(rvs, dim=2)}
+    ref = {"dq": oq, "dk": ok, "dv": ov}
+    bnd = {"dq": b_dq, "dk": b_dk, "dv": b_dv}
+    frac = {}
+    for key, val in got.items():
+        assert bool(torch.isfinite(val).all()), key
+        base = key.replace("ring_", "")
+        lim = 1.5 * bnd[base] + 1e-5 * max(1.0, float(np.max(np.abs(ref[base]))))
+        frac[key] = float(np.max(np.abs(to_host_f64(val) - ref[base]) / lim))
+    rms = {"out": rel_rms_err(to_host_f64(out), ref_o), "dv": rel_rms_err(to_host_f64(dv), ov),
+           "ring_dv": rel_rms_err(to_host_f64(got["ring_dv"]), ov)}
+    lse_err = max_abs_err(to_host_f64(lse), ref_l)
+    print(f"shifted scores d={d} shift={shift} lse~{float(np.mean(ref_l)):.1f} bound fractions",
+          " ".join(f"{k}={v:.2f}" for k, v in frac.items()), "rms",
+          " ".join(f"{k}={v:.2e}" for k, v in rms.items()), f"lse={lse_err:.2e}", flush=True)
+    assert lse_err <= TOL_BF16_LSE
+    for key, e in rms.items():
+        assert e <= TOL_BF16_REL_RMS, (key, e)
+    for key, e in frac.items():
+        assert e <= 1.0, (key, e)

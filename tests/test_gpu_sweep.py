@@ -19,7 +19,7 @@ from oracle import attention_fp64 as oa
 from paper_2507_16697_amd import inputs, ringx
 
 from parity_util import (TOL_BF16_LSE, TOL_BF16_REL_RMS, TOL_F32, max_abs_err, rel_rms_err,
-                         to_device, to_host_f64)
+                         rounding_bounds, to_device, to_host_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -123,7 +123,7 @@ def _run_case(case, grads_rms=True):
             errs[key] = (_bf16_err(got[key], ref[key]), TOL_BF16_REL_RMS)
     if store == "bf16":
         # every element also within 1.5x the bound of the path's roundings
-        b_out, b_dq, b_dk, b_dv = _rounding_bounds(x, kr, vr, ro, rl, scale)
+        b_out, b_dq, b_dk, b_dv = rounding_bounds(x, kr, vr, ro, rl, scale)
         gsum = lambda a: a.reshape(B, hkv, grp, nk, d).sum(axis=2)
         for key, b in (("out", b_out), ("dq", b_dq), ("dk", gsum(b_dk)), ("dv", gsum(b_dv))):
             lim = 1.5 * b + 1e-5 * max(1.0, float(np.max(np.abs(ref[key]))))
@@ -264,24 +264,6 @@ def test_sweep_tokenizer(case):
     assert e <= (TOL_BF16_REL_RMS if bf16 else TOL_F32), (case, e)
 
 
-def _rounding_bounds(x, kr, vr, ro, rl, scale):
-    """Element-wise bounds on the error of the bf16 path that come from its roundings alone: P and
-    dS are rounded to bf16 (relative 2^-8) before their contractions, the output is stored in
-    bf16 (another 2^-8), and D is formed from that rounded output.  Propagated with absolute
-    values through each contraction, from the fp64 quantities of the definition."""
-    u = 2.0 ** -8
-    q, do = x["q"], x["do"]
-    P = np.exp(scale * (q @ np.swapaxes(kr, -1, -2)) - rl[..., None])
-    D = np.sum(do * ro, axis=-1)
-    dS = P * (do @ np.swapaxes(vr, -1, -2) - D[..., None])
-    av = oracle.attention(q, kr, np.abs(vr), scale)[0]       # sum_j P_ij |v_j|
-    b_out = u * (av + np.abs(ro))
-    dD = np.sum(np.abs(do) * b_out, axis=-1)                   # from the rounded output
-    E = u * np.abs(dS) + P * dD[..., None]                     # |error of dS_ij|
-    b_dq = scale * (E @ np.abs(kr))
-    b_dk = scale * (np.swapaxes(E, -1, -2) @ np.abs(q))
-    b_dv = u * (np.swapaxes(P, -1, -2) @ np.abs(do))
-    return b_out, b_dq, b_dk, b_dv
 
 
 @pytest.mark.parametrize("case", _cases()[::4], ids=lambda c: "-".join(str(x) for x in c))
@@ -301,7 +283,7 @@ def test_sweep_peaked_softmax(case):
     kr, vr = np.repeat(x["k"], grp, axis=1), np.repeat(x["v"], grp, axis=1)
     ro, rl = oracle.attention(x["q"], kr, vr, scale)
     rq, rk, rv = oracle.attention_bwd(x["q"], kr, vr, ro, x["do"], rl, scale)
-    b_out, b_dq, b_dk, b_dv = _rounding_bounds(x, kr, vr, ro, rl, scale)
+    b_out, b_dq, b_dk, b_dv = rounding_bounds(x, kr, vr, ro, rl, scale)
     gsum = lambda a: a.reshape(B, hkv, grp, nk, d).sum(axis=2)
     got = {"out": to_host_f64(out), "dq": to_host_f64(dq), "dk": to_host_f64(dk),
            "dv": to_host_f64(dv)}
