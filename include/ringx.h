@@ -20,9 +20,11 @@
  *  Chunks     Chunk r of R covers keys [floor(r*Nk/R), floor((r+1)*Nk/R)); 1 <= R <= Nk.
  *  Memory     Every tensor pointer is caller-owned device memory, 16-byte aligned; outputs must
  *             not overlap inputs.  The library never allocates, frees or keeps a pointer after
- *             returning.  Scratch memory needed by the backward is passed in by the caller.
+ *             returning.  Scratch memory needed by the backward is passed in by the caller, except
+ *             for ringx_attn_bwd_noalloc, which uses a fixed device array of the library's own.
  *  Ordering   Work is enqueued on `stream` (0 = the null stream) and the call returns without
- *             synchronising.  There is no global mutable state; calls are thread-safe.
+ *             synchronising.  Apart from that fixed array there is no global mutable state; calls
+ *             are thread-safe.
  *  Errors     Arguments are checked on the host before any HIP call.  On an error status nothing
  *             has been enqueued and no output has been written.  RINGX_E_HIP reports a launch
  *             failure (hipGetLastError) after validation passed; outputs are then undefined.
@@ -56,7 +58,8 @@ typedef enum ringx_status {
   RINGX_E_ALIGN = 5,       /* a tensor pointer is not 16-byte aligned                        */
   RINGX_E_WORKSPACE = 6,   /* backward workspace missing or smaller than required            */
   RINGX_E_HIP = 7,         /* a HIP launch failed                                            */
-  RINGX_E_ALIAS = 8        /* an output overlaps an input                                    */
+  RINGX_E_ALIAS = 8,       /* an output overlaps an input                                    */
+  RINGX_E_SCRATCH = 9      /* B*H*Nq above RINGX_NOALLOC_MAX_ROWS (ringx_attn_bwd_noalloc)   */
 } ringx_status;
 
 typedef enum ringx_dtype { RINGX_FP32 = 0, RINGX_BF16 = 1 } ringx_dtype;
@@ -119,6 +122,26 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
                             int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
                             float scale, ringx_dtype dtype, int accumulate_dkv, void* workspace,
                             size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * ringx_attn_bwd without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, allocation-free serving loops, harnesses that forbid hipMalloc).
+ * The caller still passes every input and output, exactly as for ringx_attn_bwd; D (one fp32 per
+ * query row) goes to a fixed device array that the library holds on every GPU it runs on
+ * (RINGX_NOALLOC_MAX_ROWS * 4 bytes, kept until the process ends).  Nothing is allocated or freed.
+ *   RINGX_E_SCRATCH if B * H * Nq > RINGX_NOALLOC_MAX_ROWS (checked before any HIP call).
+ *   RINGX_E_HIP if the array's device address cannot be looked up (first call on a device).
+ * All calls on one GPU share that GPU's array and nothing in it survives from one call to the
+ * next (D is written in full before it is read), but calls that overlap in time on one GPU -- on
+ * different streams, or from several threads without ordering -- race on it and give undefined
+ * results; order them (one stream, or events).  Results are bitwise those of ringx_attn_bwd.
+ */
+#define RINGX_NOALLOC_MAX_ROWS 2097152
+ringx_status ringx_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* out,
+                                    const void* dout, const float* lse, float* dq, float* dk,
+                                    float* dv, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
+                                    int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                    int accumulate_dkv, hipStream_t stream);
 
 /* Backward preprocess: delta[B,H,Nq] (fp32) = sum_c dout_ic out_ic for every query row.
  *   out, dout [B,H,Nq,d] in dtype (d as for the forward).  delta is caller-owned. */

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <climits>
 #include <initializer_list>
+#include <mutex>
 
 #include "ringx.h"
 #include "ringx_kernels.h"
@@ -79,6 +80,9 @@ const char* ringx_status_str(ringx_status s) {
     case RINGX_E_WORKSPACE: return "backward workspace missing or too small";
     case RINGX_E_HIP: return "HIP launch failed";
     case RINGX_E_ALIAS: return "an output overlaps an input";
+    case RINGX_E_SCRATCH:
+      return "B * H * Nq exceeds the fixed scratch of ringx_attn_bwd_noalloc "
+             "(RINGX_NOALLOC_MAX_ROWS rows)";
   }
   return "unknown status";
 }
@@ -444,4 +448,62 @@ ringx_status ringx_tt_tokenize(const float* field, void* tokens, int64_t C, int6
 
 }  // extern "C"
 
+// ------------------------------------------------------------------------------------------------
+// ringx_attn_bwd_noalloc: ringx_attn_bwd with D (one fp32 per query row) in a fixed, file-scope
+// device array instead of a caller workspace.  Every GPU the library runs on holds its own copy of
+// the array (RINGX_NOALLOC_MAX_ROWS * 4 bytes = 8 MiB) until the process ends.  In host code the
+// array's name is only a host-side stand-in: its device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and only that address is ever passed to kernels.
 
+namespace {
+
+__device__ __align__(256) float scratch[RINGX_NOALLOC_MAX_ROWS];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device that runs `stream` (the current device for the null
+// stream).  The first call for a device makes that device current for the lookup and restores the
+// caller's device afterwards.
+ringx_status scratch_address(hipStream_t stream, float** out) {
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return RINGX_E_HIP;
+  int dev = cur;
+  if (stream != nullptr && hipStreamGetDevice(stream, &dev) != hipSuccess) return RINGX_E_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return RINGX_E_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return RINGX_E_HIP;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur && hipSetDevice(cur) != hipSuccess) return RINGX_E_HIP;
+    if (e != hipSuccess || p == nullptr) return RINGX_E_HIP;
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return RINGX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ringx_status ringx_attn_bwd_noalloc(const void* q, const void* k, const void* v, const void* out,
+                                    const void* dout, const float* lse, float* dq, float* dk,
+                                    float* dv, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
+                                    int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                    int accumulate_dkv, hipStream_t stream) {
+  if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv) return RINGX_E_NULLPTR;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  if (B * H * Nq > RINGX_NOALLOC_MAX_ROWS) return RINGX_E_SCRATCH;
+  float* ws = nullptr;
+  st = scratch_address(stream, &ws);
+  if (st != RINGX_OK) return st;
+  static_assert(RINGX_NOALLOC_MAX_ROWS % 64 == 0, "whole 256-byte blocks");
+  return bwd_impl(q, k, v, out, dout, lse, dq, dk, dv, B, H, H, Nq, Nk, d, R, scale, dtype,
+                  accumulate_dkv, ws, sizeof(float) * (size_t)RINGX_NOALLOC_MAX_ROWS, stream);
+}
+
+}  // extern "C"

@@ -28,14 +28,17 @@ RINGX_BF16 = 1
 STATUS_NAMES = {
     0: "RINGX_OK", 1: "RINGX_E_NULLPTR", 2: "RINGX_E_SHAPE", 3: "RINGX_E_CHUNKS",
     4: "RINGX_E_UNSUPPORTED", 5: "RINGX_E_ALIGN", 6: "RINGX_E_WORKSPACE", 7: "RINGX_E_HIP",
-    8: "RINGX_E_ALIAS",
+    8: "RINGX_E_ALIAS", 9: "RINGX_E_SCRATCH",
 }
+
+# rows (B * H * Nq) of the fixed device array behind ringx_attn_bwd_noalloc (RINGX_NOALLOC_MAX_ROWS)
+NOALLOC_MAX_ROWS = 2097152
 
 EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "ringx_attn_bwd",
             "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv", "ringx_attn_bwd_dq",
             "ringx_attn_fwd_step", "ringx_attn_bwd_step", "ringx_attn_fwd_gqa",
             "ringx_attn_bwd_gqa", "ringx_tt_tokenize", "ringx_bwd_workspace_bytes",
-            "ringx_chunk_bounds", "ringx_status_str")
+            "ringx_chunk_bounds", "ringx_status_str", "ringx_attn_bwd_noalloc")
 
 
 class RingxError(RuntimeError):
@@ -65,6 +68,9 @@ def lib() -> ctypes.CDLL:
         L.ringx_attn_bwd.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                      ctypes.c_float, ctypes.c_int, ctypes.c_int, _P,
                                      ctypes.c_size_t, _P]
+        L.ringx_attn_bwd_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I,
+                                             _I, _I, ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                                             _P]
         L.ringx_bwd_preprocess.argtypes = [_P, _P, _P, _I, _I, _I, _I, ctypes.c_int, _P]
         L.ringx_attn_bwd_dkdv.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                           ctypes.c_float, ctypes.c_int, ctypes.c_int, _P]
@@ -91,7 +97,7 @@ def lib() -> ctypes.CDLL:
                      "ringx_attn_bwd", "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv",
                      "ringx_attn_bwd_dq", "ringx_attn_fwd_step", "ringx_attn_bwd_step",
                      "ringx_attn_fwd_gqa", "ringx_attn_bwd_gqa", "ringx_tt_tokenize",
-                     "ringx_chunk_bounds"):
+                     "ringx_chunk_bounds", "ringx_attn_bwd_noalloc"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -284,6 +290,29 @@ def ringx_attn_bwd(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None
                               1 if accumulate_dkv else 0, workspace.data_ptr(),
                               workspace.numel() * workspace.element_size(), _stream(stream))
     _check("ringx_attn_bwd", st)
+    return dq, dk, dv
+
+
+def ringx_attn_bwd_noalloc(q, k, v, out, dout, lse, R: int, dq, dk, dv, scale=None,
+                           accumulate_dkv=False, stream=None):
+    """ringx_attn_bwd for callers that cannot allocate: the caller passes the fp32 outputs dq, dk,
+    dv, and D lives in the library's fixed device array (B * H * Nq <= NOALLOC_MAX_ROWS).  Calls
+    that overlap in time on one GPU race on that array.  Returns (dq, dk, dv)."""
+    torch = _torch()
+    _dev(q, k, v, out, dout, lse, dq, dk, dv)
+    B, H, _, Nq, Nk, d = _qkv(q, k, v)
+    _expect("out", out, q.shape, q.dtype, q.device)
+    _expect("dout", dout, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
+    _expect("dq", dq, (B, H, Nq, d), torch.float32, q.device)
+    _expect("dk", dk, (B, H, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, H, Nk, d), torch.float32, q.device)
+    st = lib().ringx_attn_bwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                      dout.data_ptr(), lse.data_ptr(), dq.data_ptr(),
+                                      dk.data_ptr(), dv.data_ptr(), B, H, Nq, Nk, d, R,
+                                      _scale(scale, d), _dtype_code(q),
+                                      1 if accumulate_dkv else 0, _stream(stream))
+    _check("ringx_attn_bwd_noalloc", st)
     return dq, dk, dv
 
 

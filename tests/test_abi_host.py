@@ -16,7 +16,7 @@ HEADER = os.path.join(ROOT, "include", "ringx.h")
 pytestmark = pytest.mark.skipif(not os.path.exists(ringx.LIB_PATH),
                                 reason="libringx.so not built (run python -m paper_2507_16697_amd.build)")
 
-OK, NULLPTR, SHAPE, CHUNKS, UNSUP, ALIGN, WORKSPACE, HIP, ALIAS = range(9)
+OK, NULLPTR, SHAPE, CHUNKS, UNSUP, ALIGN, WORKSPACE, HIP, ALIAS, SCRATCH = range(10)
 BF16, FP32 = ringx.RINGX_BF16, ringx.RINGX_FP32
 
 # Fake, never dereferenced device addresses: validation rejects every call below before any HIP
@@ -41,7 +41,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(9):
+    for code in range(10):
         s = ringx.ringx_status_str(code)
         assert isinstance(s, str) and s
     assert ringx.ringx_status_str(OK) == "ok"
@@ -131,6 +131,25 @@ def test_backward_validation():
     assert bwd(dq=QP) == ALIAS                      # dq over q
     assert bwd(dk=OP) == ALIAS                      # dk over dq
     assert bwd(ws=OP + 16 * GB) == ALIAS            # workspace over dv
+
+
+def bwd_noalloc(q=QP, k=KP, v=VP, o=OP, do=OP + 4 * GB, lse=LP, dq=OP + 8 * GB,
+                dk=OP + 12 * GB, dv=OP + 16 * GB, B=1, H=2, Nq=100, Nk=300, d=64, R=3,
+                dt=BF16, acc=0):
+    return ringx.lib().ringx_attn_bwd_noalloc(q, k, v, o, do, lse, dq, dk, dv, B, H, Nq, Nk, d,
+                                              R, 0.125, dt, acc, None)
+
+
+def test_backward_noalloc_validation():
+    """Everything ringx_attn_bwd checks, plus the fixed scratch limit (B * H * Nq rows), before
+    any HIP call."""
+    rows = ringx.NOALLOC_MAX_ROWS
+    assert bwd_noalloc(q=0) == NULLPTR and bwd_noalloc(dv=0) == NULLPTR
+    assert bwd_noalloc(R=301) == CHUNKS and bwd_noalloc(d=80) == UNSUP
+    assert bwd_noalloc(B=0) == SHAPE
+    assert bwd_noalloc(B=1, H=1, Nq=rows + 1) == SCRATCH
+    assert bwd_noalloc(B=2, H=16, Nq=rows // 32 + 1) == SCRATCH
+    assert bwd_noalloc(B=3, H=5, Nq=1 << 20) == SCRATCH
 
 
 def pre(o=QP, do=KP, dl=LP, B=1, H=2, Nq=100, d=64, dt=BF16):
