@@ -49,7 +49,15 @@ typedef struct ihipStream_t* hipStream_t;
 extern "C" {
 #endif
 
-typedef enum ringx_status {
+/* In C++ both enums are given int as their fixed underlying type, so that any int a C caller
+   passes (the ABI type of both) is a valid value of the enum on the library's side. */
+#ifdef __cplusplus
+#define RINGX_ENUM_BASE : int
+#else
+#define RINGX_ENUM_BASE
+#endif
+
+typedef enum ringx_status RINGX_ENUM_BASE {
   RINGX_OK = 0,
   RINGX_E_NULLPTR = 1,     /* a required pointer is NULL                                     */
   RINGX_E_SHAPE = 2,       /* B, H, Nq, Nk < 1, a size overflows, or scale not finite and > 0 */
@@ -62,7 +70,7 @@ typedef enum ringx_status {
   RINGX_E_SCRATCH = 9      /* B*H*Nq above RINGX_NOALLOC_MAX_ROWS (ringx_attn_bwd_noalloc)   */
 } ringx_status;
 
-typedef enum ringx_dtype { RINGX_FP32 = 0, RINGX_BF16 = 1 } ringx_dtype;
+typedef enum ringx_dtype RINGX_ENUM_BASE { RINGX_FP32 = 0, RINGX_BF16 = 1 } ringx_dtype;
 
 /*
  * Ring-chunked forward with the Eq. (5) merge fused (Sec. III-A, Eqs. (1)-(5)).
@@ -255,8 +263,9 @@ size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, i
 /* Key range [*lo, *hi) of chunk r (lo = floor(r*Nk/R)).  Host only; no HIP call. */
 ringx_status ringx_chunk_bounds(int64_t Nk, int64_t R, int64_t r, int64_t* lo, int64_t* hi);
 
-/* Static, NUL-terminated description of a status code. */
-const char* ringx_status_str(ringx_status s);
+/* Static, NUL-terminated description of a status code (any int: values that are not a
+   ringx_status give "unknown status"). */
+const char* ringx_status_str(int status);
 
 #ifdef __cplusplus
 }

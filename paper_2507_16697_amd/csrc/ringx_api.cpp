@@ -69,8 +69,9 @@ ringx_status hip_status(hipError_t e) { return e == hipSuccess ? RINGX_OK : RING
 
 extern "C" {
 
-const char* ringx_status_str(ringx_status s) {
-  switch (s) {
+const char* ringx_status_str(int status) {
+  // an int, not the enum: a C caller may pass any value, and an out-of-range enum is undefined
+  switch (status) {
     case RINGX_OK: return "ok";
     case RINGX_E_NULLPTR: return "a required pointer is NULL";
     case RINGX_E_SHAPE: return "invalid shape, size overflow or scale";

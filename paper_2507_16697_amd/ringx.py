@@ -20,7 +20,9 @@ import ctypes
 import math
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libringx.so")
+# RINGX_LIB names another build of the same library (e.g. the host-sanitizer build of the tests)
+LIB_PATH = os.environ.get("RINGX_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                       "libringx.so")
 
 RINGX_FP32 = 0
 RINGX_BF16 = 1

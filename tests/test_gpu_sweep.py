@@ -4,7 +4,7 @@
 or 4 query heads, ragged query (1-419) and key (1-1099) lengths, chunk counts from 1 up to Nk, bf16
 at d = 64 / 128 and fp32 at any d in 1..128.  Each runs the grouped forward and backward (plain
 multi-head attention when the group is 1), and every third one also the ring-step forward over
-its chunks.  Bars: fp32 max abs 1e-5 (gradients relative to max(1, max |ref|)); bf16 max abs
+its chunks.  Bars: fp32 max abs 1e-5; bf16 max abs
 relative to the reference RMS 2e-2, lse max abs 2e-2.
 """
 
@@ -113,10 +113,7 @@ def _run_case(case, grads_rms=True):
     errs = {}
     for key in got:
         if store == "fp32":
-            e = max_abs_err(got[key], ref[key])
-            if key in ("dq", "dk", "dv"):
-                e /= max(1.0, float(np.max(np.abs(ref[key]))))
-            errs[key] = (e, TOL_F32)
+            errs[key] = (max_abs_err(got[key], ref[key]), TOL_F32)
         elif key.endswith("lse"):
             errs[key] = (max_abs_err(got[key], ref[key]), TOL_BF16_LSE)
         elif grads_rms or key not in ("dq", "dk", "dv"):
@@ -147,10 +144,9 @@ def _inputs(case):
     return x, g, float(np.float32(1 / math.sqrt(d)))
 
 
-def _err(store, key, got, ref, grad=False):
+def _err(store, key, got, ref):
     if store == "fp32":
-        e = max_abs_err(got, ref)
-        return e / max(1.0, float(np.max(np.abs(ref)))) if grad else e, TOL_F32
+        return max_abs_err(got, ref), TOL_F32
     if key.endswith("lse"):
         return max_abs_err(got, ref), TOL_BF16_LSE
     return _bf16_err(got, ref), TOL_BF16_REL_RMS
@@ -220,9 +216,9 @@ def test_sweep_ring_backward(case):
     torch.cuda.synchronize()
     ro, rl = oracle.attention(x["q"], x["k"], x["v"], scale)
     rq, rk, rv = oracle.attention_bwd(x["q"], x["k"], x["v"], ro, x["do"], rl, scale)
-    errs = {"dq": _err(store, "dq", to_host_f64(dq), rq, grad=True),
-            "dk": _err(store, "dk", to_host_f64(dk), rk, grad=True),
-            "dv": _err(store, "dv", to_host_f64(dv), rv, grad=True)}
+    errs = {"dq": _err(store, "dq", to_host_f64(dq), rq),
+            "dk": _err(store, "dk", to_host_f64(dk), rk),
+            "dv": _err(store, "dv", to_host_f64(dv), rv)}
     print(case, " ".join(f"{k}={e:.2e}" for k, (e, _) in errs.items()), flush=True)
     for key, (e, tol) in errs.items():
         assert e <= tol, (case, key, e)
@@ -294,7 +290,7 @@ def test_sweep_peaked_softmax(case):
     for key in got:
         err = np.abs(got[key] - ref[key])
         if store == "fp32":
-            worst[key] = float(np.max(err)) / max(1.0, float(np.max(np.abs(ref[key])))) / TOL_F32
+            worst[key] = float(np.max(err)) / TOL_F32
         else:
             # 1.5x the rounding bound, plus fp32 accumulation noise
             lim = 1.5 * bound[key] + 1e-5 * max(1.0, float(np.max(np.abs(ref[key]))))
