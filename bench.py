@@ -57,34 +57,151 @@ def load_traffic(kernel, workload, src_hash):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(t, w, rows):
-    """The fp64 oracle on host cores: head 0, the first `rows` queries against all keys,
-    forward + backward.  Returns the baseline record (TFLOP/s of the same flop convention)."""
+def _oracle_fwd_bwd(inputs, oracle, t, w, h, rows, with_bwd=True):
+    """Seconds of the fp64 oracle, as it stands, on head h: queries 0..rows-1 against all keys,
+    forward (+ backward).  Returns (seconds, flops of the 4 (+8) * rows * Nk * d convention)."""
     import numpy as np
-    from threadpoolctl import threadpool_info
+
+    store = w.dtype
+    q = inputs.to_f64(t["q"][0, h, :rows], store)
+    k = inputs.to_f64(t["k"][0, h], store)
+    v = inputs.to_f64(t["v"][0, h], store)
+    t0 = time.perf_counter()
+    o, lse = oracle.head_attention(q, k, v, w.scale)
+    flops = 4.0 * rows * w.Nk * w.d
+    if with_bwd:
+        do = inputs.to_f64(t["do"][0, h, :rows], store)
+        D = oracle.head_bwd_preprocess(o, do)
+        dq, dk, _ = oracle.head_attention_bwd(q, k, v, do, lse, D, w.scale)
+        assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk))
+        flops = 12.0 * rows * w.Nk * w.d
+    return time.perf_counter() - t0, flops
+
+
+def cpu_baseline(t, w, rows, full_head=False, others=True):
+    """The fp64 oracle on the host cores this process may use (len(os.sched_getaffinity(0)), the
+    BLAS library held to that many threads; numpy's elementwise work is single-threaded).
+
+    The headline sample: head 0 of the timed workload, its first `rows` queries against all keys,
+    forward + backward; the whole step's oracle time is that times (Nq / rows) * B * H (every row
+    of every head costs the same), reported as an extrapolation.  Beside it: the tiny exactness
+    case in full (forward, on all cores and on one core) and one full head of the 16k single shard
+    (forward + backward, extrapolated to its 16 heads).  full_head=True also times one full head
+    of the timed workload and the whole single shard (minutes)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     import oracle
     from paper_2507_16697_amd import inputs
 
-    q = inputs.to_f64(t["q"][0, 0, :rows], "bf16")
-    k = inputs.to_f64(t["k"][0, 0], "bf16")
-    v = inputs.to_f64(t["v"][0, 0], "bf16")
-    do = inputs.to_f64(t["do"][0, 0, :rows], "bf16")
-    t0 = time.perf_counter()
-    o, lse = oracle.head_attention(q, k, v, w.scale)
-    D = oracle.head_bwd_preprocess(o, do)
-    dq, dk, dv = oracle.head_attention_bwd(q, k, v, do, lse, D, w.scale)
-    sec = time.perf_counter() - t0
-    assert np.all(np.isfinite(dq)) and np.all(np.isfinite(dk))
-    flops = 12.0 * rows * w.Nk * w.d
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {
-        "value": flops / sec / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-        "seconds": sec,
-        "sample": f"fp64 oracle, head 0 of {w.name}: queries 0..{rows - 1} against all {w.Nk} "
-                  f"keys, forward + backward, {flops:.3e} flops (12*rows*Nk*d)",
-        "cpu": _cpu_model(),
-    }
+    cores = len(os.sched_getaffinity(0))
+    rec = {"unit": "TFLOP/s", "kind": "oracle", "cores": cores, "cpu": _cpu_model()}
+    with threadpool_limits(limits=cores, user_api="blas"):
+        blas = max([p.get("num_threads", 1) for p in threadpool_info()
+                    if p.get("user_api") == "blas"] or [1])
+        sec, flops = _oracle_fwd_bwd(inputs, oracle, t, w, 0, rows)
+        steps = w.B * w.H * (w.Nq / rows)
+        rec.update({
+            "value": flops / sec / 1e12, "seconds": sec, "blas_threads": blas,
+            "sample": f"fp64 oracle, head 0 of {w.name}: queries 0..{rows - 1} against all "
+                      f"{w.Nk} keys, forward + backward, {flops:.3e} flops (12*rows*Nk*d)",
+            "step_seconds_extrapolated": sec * steps,
+            "extrapolation": f"x {steps:g} = (Nq / rows) * B * H: every row of every head costs "
+                             "the same",
+        })
+        extra = {}
+        if not others:
+            return rec
+        w1 = inputs.WORKLOADS["exact_fp32_n1k"]
+        t1 = inputs.make_workload(w1.name)
+        s_all = sum(_oracle_fwd_bwd(inputs, oracle, t1, w1, h, w1.Nq, with_bwd=False)[0]
+                    for h in range(w1.H))
+        with threadpool_limits(limits=1, user_api="blas"):
+            s_one = sum(_oracle_fwd_bwd(inputs, oracle, t1, w1, h, w1.Nq, with_bwd=False)[0]
+                        for h in range(w1.H))
+        f1 = 4.0 * w1.B * w1.H * w1.Nq * w1.Nk * w1.d
+        extra[w1.name] = {"pass": "fwd", "seconds": s_all, "tflops": f1 / s_all / 1e12,
+                          "seconds_1_core": s_one, "tflops_1_core": f1 / s_one / 1e12,
+                          "what": "in full (every head, every row)"}
+        w2 = inputs.WORKLOADS["shard_n16k_d64"]
+        t2 = inputs.make_workload(w2.name)
+        s2, f2 = _oracle_fwd_bwd(inputs, oracle, t2, w2, 0, w2.Nq)
+        extra[w2.name] = {"pass": "fwd+bwd", "seconds_head0": s2, "tflops": f2 / s2 / 1e12,
+                          "seconds_extrapolated": s2 * w2.B * w2.H,
+                          "what": f"head 0 in full, x {w2.B * w2.H} heads extrapolated"}
+        if full_head:
+            sf, ff = _oracle_fwd_bwd(inputs, oracle, t, w, 0, w.Nq)
+            extra[w.name + "_head0_full"] = {
+                "pass": "fwd+bwd", "seconds": sf, "tflops": ff / sf / 1e12,
+                "step_seconds_extrapolated": sf * w.B * w.H,
+                "what": f"head 0 in full, x {w.B * w.H} heads extrapolated"}
+            sa = s2 + sum(_oracle_fwd_bwd(inputs, oracle, t2, w2, h, w2.Nq)[0]
+                          for h in range(1, w2.H))
+            extra[w2.name]["seconds_full"] = sa
+        rec["other_configs"] = extra
+    return rec
+
+
+def input_sha256(t):
+    """SHA-256 of every generated input tensor (host storage bytes), computed in parallel."""
+    import concurrent.futures
+
+    from paper_2507_16697_amd import inputs
+
+    names = sorted(t)
+    with concurrent.futures.ThreadPoolExecutor(len(names)) as ex:
+        digests = list(ex.map(lambda n: inputs.sha256_of(t[n]), names))
+    return dict(zip(names, digests))
+
+
+class ClockSampler:
+    """Samples the GPU's shader clock (rocm-smi) on a host thread while the timed steps run."""
+
+    def __init__(self, period=0.5):
+        import threading
+        self.period = period
+        self.samples = []
+        self.error = None
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        import re
+        import subprocess
+        r = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
+                           text=True, timeout=10)
+        data = json.loads(r.stdout)
+        for card in data.values():
+            for key, val in card.items():
+                if "sclk" in key.lower():
+                    m = re.search(r"(\d+)\s*Mhz", str(val), re.I)
+                    if m:
+                        return int(m.group(1))
+        raise ValueError("no sclk in rocm-smi output")
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._read())
+            except Exception as e:   # a missing or failing tool leaves the record empty
+                self.error = f"{type(e).__name__}: {e}"[:200]
+                return
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        self._thread.join(timeout=15)
+
+    def record(self):
+        if not self.samples:
+            return {"source": "rocm-smi --showclocks", "mhz": None, "error": self.error}
+        x = sorted(self.samples)
+        return {"source": "rocm-smi --showclocks, sampled every 0.5 s over the timed steps",
+                "samples": len(x), "mhz_min": x[0], "mhz_median": x[len(x) // 2],
+                "mhz_max": x[-1]}
 
 
 def _cpu_model():
@@ -121,11 +238,12 @@ def _stats(ms, flops):
 
 
 def other_shapes(torch, np, inputs, ringx, stream, dev):
-    """Timings of the other paper-shaped workloads: the 16k single shard (fwd+bwd, d=64), the
-    turbulence tokens (fwd, d=64, inputs from the host recipe: 256^3 field, 4^3 patches, seeded
-    embedding and projections) and the 524k long step (fwd+bwd, d=128, plus the standalone merge).
-    The i.i.d. workloads are drawn on the device (torch's seeded generator, the workload's
-    distribution) so that the run stays short; their parity tests use the host recipe."""
+    """Timings of the other paper-shaped workloads: the 16k single shard (fwd+bwd, d=64) and the
+    turbulence tokens (fwd, d=64: 256^3 field, 4^3 patches, seeded embedding and projections),
+    both from the host recipe, and the 524k long step (fwd+bwd, d=128, plus the standalone
+    merge), whose 2.4e9 inputs are drawn on the device (torch's seeded generator, the workload's
+    distribution; labelled so in the record) so that the run stays short; its parity tests use
+    the host recipe."""
     res = {}
     gen = torch.Generator(device=dev)
 
@@ -164,7 +282,13 @@ def other_shapes(torch, np, inputs, ringx, stream, dev):
         return r
 
     w = inputs.WORKLOADS["shard_n16k_d64"]
-    res[w.name] = fwd_bwd(w, iid(w, w.seed), 3, 10)
+    tt = inputs.make_workload(w.name)
+    x = {n: torch.from_numpy(np.ascontiguousarray(tt[n]).view(np.int16)).to(dev)
+         .view(torch.bfloat16) for n in ("q", "k", "v", "do")}
+    del tt
+    res[w.name] = fwd_bwd(w, x, 3, 10)
+    res[w.name]["inputs"] = "host recipe"
+    del x
     log(f"[bench] {w.name}: {res[w.name]['ms_median']:.2f} ms/step, "
         f"{res[w.name]['tflops_median']:.1f} TFLOP/s")
 
@@ -216,6 +340,9 @@ def main():
     ap.add_argument("--workload", default="ring8_nk262k_d128")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8192)
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="also time the oracle on one full head of the workload and on the whole "
+                         "16k single shard (minutes of host time)")
     ap.add_argument("--no-merge", action="store_true")
     ap.add_argument("--no-tokenizer", action="store_true",
                     help="skip the multi-fidelity tokenizer measurement (1024^3 x 4 field)")
@@ -261,6 +388,7 @@ def main():
     t0 = time.time()
     t = inputs.make_workload(w.name)
     log(f"[bench] inputs ready in {time.time() - t0:.1f}s; moving to HBM")
+    sha = input_sha256(t)
     dev = torch.device("cuda:0")
 
     def to_dev(a):
@@ -302,11 +430,12 @@ def main():
     K = args.steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for s_ in range(K):
-        step(ev[s_])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
+    with ClockSampler() as clock:
+        wall0 = time.perf_counter()
+        for s_ in range(K):
+            step(ev[s_])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
     total_ms = ev[0][0].elapsed_time(ev[K - 1][4])
 
     def avg(i, j):
@@ -498,6 +627,9 @@ def main():
         "kernels": kernels,
         "gpu": torch.cuda.get_device_name(0),
         "hip": torch.version.hip,
+        "sclk": clock.record(),
+        "inputs": {"recipe": f"seeded host generator, {w.name} (per-slab PCG64 streams)",
+                   "sha256": sha},
         # the paper's own figures, system-level on other hardware: context, not a target (the
         # paper reports no single-GPU throughput for this kernel path, so vs_baseline is null)
         "paper_context": {
@@ -508,7 +640,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log(f"[bench] cpu baseline: oracle on {args.cpu_rows} query rows of head 0")
-        result["cpu_baseline"] = cpu_baseline(t, w, args.cpu_rows)
+        result["cpu_baseline"] = cpu_baseline(t, w, args.cpu_rows, full_head=args.cpu_full)
         log(f"[bench] cpu baseline {result['cpu_baseline']['seconds']:.1f}s")
     else:
         result["cpu_baseline"] = None

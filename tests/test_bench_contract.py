@@ -38,10 +38,30 @@ def test_cpu_baseline_record():
     t = inputs.make_iid(1, 1, 4, w.Nk, w.d, seed=5, std=0.5, store="bf16", with_do=True)
     rec = bench.cpu_baseline(t, w, rows=4)
     assert rec["kind"] == "oracle" and rec["unit"] == "TFLOP/s"
-    assert rec["value"] > 0 and rec["seconds"] > 0 and rec["cores"] >= 1
+    assert rec["value"] > 0 and rec["seconds"] > 0
+    assert rec["cores"] == len(os.sched_getaffinity(0)) and 1 <= rec["blas_threads"]
     assert "queries 0..3" in rec["sample"] and str(w.Nk) in rec["sample"]
     # the same flop convention as the GPU figure: 12 * rows * Nk * d
     assert rec["value"] == pytest.approx(12.0 * 4 * w.Nk * w.d / rec["seconds"] / 1e12)
+    # the whole step, extrapolated from the sample: every row of every head costs the same
+    assert rec["step_seconds_extrapolated"] == pytest.approx(rec["seconds"] * w.H * w.Nq / 4)
+    other = rec["other_configs"]
+    c1 = other["exact_fp32_n1k"]
+    assert c1["seconds"] > 0 and c1["seconds_1_core"] > 0 and c1["pass"] == "fwd"
+    c2 = other["shard_n16k_d64"]
+    assert c2["seconds_extrapolated"] == pytest.approx(16 * c2["seconds_head0"])
+
+
+def test_input_hashes_identify_the_inputs():
+    bench = _bench()
+    from paper_2507_16697_amd import inputs
+
+    t = inputs.make_iid(1, 2, 8, 16, 64, seed=9, store="bf16")
+    a = bench.input_sha256(t)
+    b = bench.input_sha256(inputs.make_iid(1, 2, 8, 16, 64, seed=9, store="bf16"))
+    c = bench.input_sha256(inputs.make_iid(1, 2, 8, 16, 64, seed=10, store="bf16"))
+    assert set(a) == {"q", "k", "v", "do"} and a == b
+    assert all(a[n] != c[n] for n in a) and all(len(x) == 64 for x in a.values())
 
 
 def test_traffic_is_reported_only_for_its_source():
