@@ -6,7 +6,8 @@
 // ((c p + iz) p + iy) p + ix).
 //
 // HBM-bound: the filter windows do not overlap, so every subdomain cell is read once and every
-// token feature written once.  For k a power of two (every filter of Table III) a wave streams
+// token feature written once.  The unfiltered crop with patch 1 (Table III's filter 1) is a copy
+// with one thread per cell and contiguous per-token stores.  For k a power of two a wave streams
 // 256 consecutive cells of a row, 4 per lane, through the k^2 rows of its windows and accumulates
 // in registers; the k cells of a window are then summed within the lane (k <= 4) or across k/4
 // lanes by butterfly shuffles.  Other k take a plain kernel with one thread per filtered cell.
@@ -155,6 +156,50 @@ __global__ __launch_bounds__(kTokThreads) void tt_tokenize_rows_kernel(
   }
 }
 
+// The unfiltered crop (k = 1) with patch 1: token t = subdomain cell (z, y, x), x fastest, and its
+// C features are the C channels of that cell.  One thread per cell: the channel loads of
+// consecutive threads are consecutive cells of a row (coalesced), and each thread writes its C
+// features as one contiguous run (16-byte stores of 4 channels when C is a multiple of 4), so
+// every output line is written whole by neighbouring threads.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(kTokThreads) void tt_crop_kernel(
+    const float* __restrict__ field, void* __restrict__ tokens, int C, int D, int H, int W,
+    int sz, int sy, int sx, int z0, int y0, int x0) {
+  const int64_t n = (int64_t)sz * sy * sx;
+  const int64_t i = (int64_t)blockIdx.x * kTokThreads + threadIdx.x;
+  if (i >= n) return;
+  const int x = (int)(i % sx);
+  const int64_t r = i / sx;
+  const int y = (int)(r % sy);
+  const int z = (int)(r / sy);
+  int zz = z0 + z, yy = y0 + y, xx = x0 + x;
+  zz -= zz >= D ? D : 0;
+  yy -= yy >= H ? H : 0;
+  xx -= xx >= W ? W : 0;
+  const int64_t plane = (int64_t)D * H * W;
+  const float* src = field + ((int64_t)zz * H + yy) * W + xx;
+  if ((C & 3) == 0) {
+    for (int c = 0; c < C; c += 4) {
+      const f32x4 v = {src[c * plane], src[(c + 1) * plane], src[(c + 2) * plane],
+                       src[(c + 3) * plane]};
+      if constexpr (OUT_BF16) {
+        u32x2 w2;
+        w2[0] = pack_bf16x2(v[0], v[1]);
+        w2[1] = pack_bf16x2(v[2], v[3]);
+        *reinterpret_cast<u32x2*>(reinterpret_cast<__bf16*>(tokens) + i * C + c) = w2;
+      } else {
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(tokens) + i * C + c) = v;
+      }
+    }
+  } else {
+    for (int c = 0; c < C; ++c) {
+      const float v = src[c * plane];
+      if constexpr (OUT_BF16) reinterpret_cast<__bf16*>(tokens)[i * C + c] = (__bf16)v;
+      else reinterpret_cast<float*>(tokens)[i * C + c] = v;
+    }
+  }
+}
+
 template <int K>
 hipError_t launch_rows(const TokArgs& a) {
   const int64_t rows = a.C * a.gz * a.gy;
@@ -171,6 +216,20 @@ hipError_t launch_rows(const TokArgs& a) {
 }  // namespace
 
 hipError_t launch_tt_tokenize(const TokArgs& a) {
+  if (a.k == 1 && a.p == 1) {
+    // the unfiltered crop: one thread per subdomain cell (the weight of a 1-cell window is 1)
+    const int64_t n = a.gz * a.gy * a.gx;
+    const dim3 grid((uint32_t)((n + kTokThreads - 1) / kTokThreads));
+    if (a.out_bf16)
+      hipLaunchKernelGGL(tt_crop_kernel<true>, grid, dim3(kTokThreads), 0, a.stream, a.field,
+                         a.tokens, (int)a.C, (int)a.D, (int)a.H, (int)a.W, (int)a.gz, (int)a.gy,
+                         (int)a.gx, (int)a.z0, (int)a.y0, (int)a.x0);
+    else
+      hipLaunchKernelGGL(tt_crop_kernel<false>, grid, dim3(kTokThreads), 0, a.stream, a.field,
+                         a.tokens, (int)a.C, (int)a.D, (int)a.H, (int)a.W, (int)a.gz, (int)a.gy,
+                         (int)a.gx, (int)a.z0, (int)a.y0, (int)a.x0);
+    return hipGetLastError();
+  }
   // the row kernel needs 4-cell lane groups inside the subdomain row: sx % 4 == 0
   const int64_t sx = a.gx * a.k;
   const int64_t rows = a.C * a.gz * a.gy;
