@@ -261,14 +261,14 @@ def other_shapes(torch, np, inputs, ringx, stream, dev):
         B, H, Nq, Nk, d, R = w.B, w.H, w.Nq, w.Nk, w.d, w.R
         out = torch.empty_like(q)
         lse = torch.empty((B, H, Nq), dtype=torch.float32, device=dev)
-        delta = torch.empty_like(lse)
+        delta = torch.empty((2, B, H, Nq), dtype=torch.float32, device=dev)
         dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=dev)
         dk = torch.empty((B, H, Nk, d), dtype=torch.float32, device=dev)
         dv = torch.empty_like(dk)
 
         def step():
             ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
-            ringx.ringx_bwd_preprocess(out, do, delta=delta, stream=stream)
+            ringx.ringx_bwd_preprocess(out, do, lse, delta=delta, stream=stream)
             ringx.ringx_attn_bwd_dkdv(q, k, v, do, lse, delta, R, scale=w.scale, dk=dk, dv=dv,
                                       stream=stream)
             ringx.ringx_attn_bwd_dq(q, k, v, do, lse, delta, R, scale=w.scale, dq=dq,
@@ -405,7 +405,7 @@ def main():
                      dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
-    delta = ws[: B * H * Nq * 4].view(torch.float32).view(B, H, Nq)
+    delta = ws[: 2 * B * H * Nq * 4].view(torch.float32).view(2, B, H, Nq)
 
     def step(ev=None):
         # one step = ringx_attn_fwd + ringx_attn_bwd; the backward is issued as its three stages
@@ -414,7 +414,7 @@ def main():
         if marks[0]: marks[0].record(stream)
         ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
         if marks[1]: marks[1].record(stream)
-        ringx.ringx_bwd_preprocess(out, do, delta=delta, stream=stream)
+        ringx.ringx_bwd_preprocess(out, do, lse, delta=delta, stream=stream)
         if marks[2]: marks[2].record(stream)
         ringx.ringx_attn_bwd_dkdv(q, k, v, do, lse, delta, R, scale=w.scale, dk=dk, dv=dv,
                                   stream=stream)

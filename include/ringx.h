@@ -121,7 +121,8 @@ ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void*
  *   dk, dv [B,H,Nk,d] fp32 -- overwritten, or added to when accumulate_dkv != 0 (as dK/dV
  *   travelling around a ring collect the contributions of other query shards).
  *   workspace/workspace_bytes -- device scratch of at least ringx_bwd_workspace_bytes(...) bytes,
- *   16-byte aligned, owned by the caller; it receives D; contents on entry are ignored.
+ *   16-byte aligned, owned by the caller; it receives the per-row statistics of
+ *   ringx_bwd_preprocess (D and nl); contents on entry are ignored.
  *   R -- chunk count: no key tile straddles a chunk boundary; results do not depend on R beyond
  *   rounding.  dq, dk and dv are bitwise reproducible.
  */
@@ -134,13 +135,14 @@ ringx_status ringx_attn_bwd(const void* q, const void* k, const void* v, const v
 /*
  * ringx_attn_bwd without a workspace argument, for callers that cannot allocate device memory
  * (code under HIP graph capture, allocation-free serving loops, harnesses that forbid hipMalloc).
- * The caller still passes every input and output, exactly as for ringx_attn_bwd; D (one fp32 per
- * query row) goes to a fixed device array that the library holds on every GPU it runs on
- * (RINGX_NOALLOC_MAX_ROWS * 4 bytes, kept until the process ends).  Nothing is allocated or freed.
+ * The caller still passes every input and output, exactly as for ringx_attn_bwd; the per-row
+ * statistics (D and nl, two fp32 per query row) go to a fixed device array that the library holds
+ * on every GPU it runs on (RINGX_NOALLOC_MAX_ROWS * 8 bytes = 16 MiB, kept until the process ends).
+ * Nothing is allocated or freed.
  *   RINGX_E_SCRATCH if B * H * Nq > RINGX_NOALLOC_MAX_ROWS (checked before any HIP call).
  *   RINGX_E_HIP if the array's device address cannot be looked up (first call on a device).
  * All calls on one GPU share that GPU's array and nothing in it survives from one call to the
- * next (D is written in full before it is read), but calls that overlap in time on one GPU -- on
+ * next (the statistics are written in full before they are read), but calls that overlap in time on one GPU -- on
  * different streams, or from several threads without ordering -- race on it and give undefined
  * results; order them (one stream, or events).  Results are bitwise those of ringx_attn_bwd.
  */
@@ -151,16 +153,21 @@ ringx_status ringx_attn_bwd_noalloc(const void* q, const void* k, const void* v,
                                     int64_t d, int64_t R, float scale, ringx_dtype dtype,
                                     int accumulate_dkv, hipStream_t stream);
 
-/* Backward preprocess: delta[B,H,Nq] (fp32) = sum_c dout_ic out_ic for every query row.
- *   out, dout [B,H,Nq,d] in dtype (d as for the forward).  delta is caller-owned. */
-ringx_status ringx_bwd_preprocess(const void* out, const void* dout, float* delta, int64_t B,
-                                  int64_t H, int64_t Nq, int64_t d, ringx_dtype dtype,
-                                  hipStream_t stream);
+/* Backward preprocess: the per-row statistics of the recompute backward, delta [2,B,H,Nq] fp32:
+ *   delta[0] = D_i = sum_c dout_ic out_ic;
+ *   delta[1] = nl_i = -lse_i * log2(e), the row's log-sum-exp as the offset of the base-2
+ *              exponent the kernels form, P_ij = 2^(scale log2(e) q_i.k_j + nl_i) (stored once so
+ *              that no kernel multiplies it per score element).
+ *   out, dout [B,H,Nq,d] in dtype (d as for the forward); lse [B,H,Nq] fp32 (natural log, from
+ *   ringx_attn_fwd or ringx_lse_merge).  delta is caller-owned and must not overlap the inputs. */
+ringx_status ringx_bwd_preprocess(const void* out, const void* dout, const float* lse,
+                                  float* delta, int64_t B, int64_t H, int64_t Nq, int64_t d,
+                                  ringx_dtype dtype, hipStream_t stream);
 
 /* Gradients of the keys and values (the part a RingX group reduces across ranks): for every key
  * j of every chunk, dV_j = sum_i P_ij dout_i and dK_j = scale sum_i dS_ij q_i over all Nq queries,
- * using lse and delta from ringx_bwd_preprocess.  dk, dv [B,H,Nk,d] fp32, overwritten or added
- * to (accumulate_dkv != 0). */
+ * using lse and delta [2,B,H,Nq] from ringx_bwd_preprocess (with the same lse).  dk, dv [B,H,Nk,d]
+ * fp32, overwritten or added to (accumulate_dkv != 0). */
 ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, const void* dout,
                                  const float* lse, const float* delta, float* dk, float* dv,
                                  int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
@@ -168,7 +175,8 @@ ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
                                  hipStream_t stream);
 
 /* Gradient of the queries (the part each rank accumulates over all ring steps):
- * dQ_i = scale sum_j dS_ij k_j over the keys of every chunk.  dq [B,H,Nq,d] fp32, overwritten. */
+ * dQ_i = scale sum_j dS_ij k_j over the keys of every chunk, with lse and delta [2,B,H,Nq] as for
+ * ringx_attn_bwd_dkdv.  dq [B,H,Nq,d] fp32, overwritten. */
 ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, const void* dout,
                                const float* lse, const float* delta, float* dq, int64_t B,
                                int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
@@ -197,8 +205,8 @@ ringx_status ringx_attn_fwd_step(const void* q, const void* k, const void* v, fl
 /*
  * One ring step of the backward (Sec. III-A, "Communication scheme": the K/V chunk's gradients
  * are computed at the step that holds the chunk and sent back to its owner; dQ accumulates over
- * the N steps).  With lse and delta of the whole sequence (the merged lse, D from
- * ringx_bwd_preprocess), for the one chunk k, v [B,H,Nk,d]:
+ * the N steps).  With lse and delta of the whole sequence (the merged lse, and delta [2,B,H,Nq]
+ * from ringx_bwd_preprocess with it), for the one chunk k, v [B,H,Nk,d]:
  *   dk, dv [B,H,Nk,d] fp32 -- the chunk's gradients, overwritten or added to
  *   (accumulate_dkv != 0);
  *   dq_acc [B,H,Nq,d] fp32 -- the chunk's contribution to dQ, added to the running sum

@@ -10,7 +10,8 @@
 // dV^T accumulate in registers.  Per 32-query block:
 //   S   = Q K^T           A = Q rows (LDS),  B = K rows (registers)      -> lane = key
 //   D-dP = D + dO (-V)^T  A = dO rows (LDS), B = -V rows (registers), accumulators start at D
-//   P   = exp2(S*scale*log2e - lse_i*log2e),  -dS = P (D - dP)           (fp32)
+//   P   = exp2(S*scale*log2e + nl_i),  -dS = P (D - dP)                   (fp32; nl_i = -lse_i*log2e
+//                                                                        from the preprocess)
 //   dV^T += dO^T P        A = dO^T by transposed LDS reads, B = P from registers
 //   -dK^T += Q^T (-dS)    A = Q^T by transposed LDS reads,  B = -dS from registers
 // (negating V and dK are exact, and let the matrix cores subtract D).
@@ -20,7 +21,7 @@
 // at a time, each beside half of one of the P/dS elements 8..15 of block j; phase 2 issues the 16
 // dV/dK products of block j, each beside half of one of the elements 0..7 of block j+1.  LDS
 // operands are read 16 products ahead.  Every vector instruction then hides behind a matrix
-// product.  Q, dO, lse and D rotate through a four-stage LDS ring filled by direct global->LDS
+// product.  Q, dO, nl and D rotate through a four-stage LDS ring filled by direct global->LDS
 // loads three tiles ahead; one barrier per tile.  Rows past Nq in a head's last tile are clamped
 // copies whose dO row and D are zeroed in LDS, so they add nothing; key lanes past the chunk end
 // only feed their own dK/dV columns, which are not written.  dQ is computed by the
@@ -56,14 +57,14 @@ struct DkvCfg {
   static constexpr int kCT = D / 32;
   static constexpr int kQTile = kBQ * kRowBytes;   // bytes of one Q or dO tile
   static constexpr int kLoads = kQTile / (kThreads * 16);   // 16-byte loads per thread per tile
-  // one stage of the ring: Q tile, dO tile, lse[kBQ], D[kBQ]
+  // one stage of the ring: Q tile, dO tile, nl[kBQ], D[kBQ]
   static constexpr int kOffO = kQTile;
   static constexpr int kOffL = 2 * kQTile;
   static constexpr int kOffD = kOffL + kBQ * 4;
   static constexpr int kStage = kOffD + kBQ * 4;
   static constexpr int kStages = 4;
   static constexpr int kLds = kStages * kStage;
-  // vector-memory operations one tile puts in flight per wave (waves 0 and 1 add lse / D)
+  // vector-memory operations one tile puts in flight per wave (waves 0 and 1 add nl / D)
   static constexpr int kTileOps = 2 * kLoads;
   static_assert(kLoads >= 1 && kQTile == kLoads * kThreads * 16, "whole tiles per load round");
 };
@@ -89,7 +90,7 @@ __device__ __forceinline__ int eoff(int row, int col) {
 template <int D>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-    const __bf16* __restrict__ dout, const float* __restrict__ lse,
+    const __bf16* __restrict__ dout, const float* __restrict__ nl,
     const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BHkv,
     int H, int grp, int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale,
     int accumulate) {
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
   const int64_t qh0 = (bh / (H / grp)) * H + (bh % (H / grp)) * grp;
   const char* qb = reinterpret_cast<const char*>(q + qh0 * Nq * D);
   const char* ob = reinterpret_cast<const char*>(dout + qh0 * Nq * D);
-  const float* lseb = lse + qh0 * Nq;
+  const float* nlb = nl + qh0 * Nq;
   const float* deltab = delta + qh0 * Nq;
   const int nqt = (int)((Nq + C::kBQ - 1) / C::kBQ);
   const int ntiles = grp * nqt;
@@ -146,7 +147,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
         load_lds16_s(qs + u * kRound, goff, dst + u * kRound);
         load_lds16_s(os + u * kRound, goff, dst + C::kOffO + u * kRound);
       }
-      if (wave == 0) load_lds4_s(lseb + ld_row, 4 * lane, dst - wdst + C::kOffL);
+      if (wave == 0) load_lds4_s(nlb + ld_row, 4 * lane, dst - wdst + C::kOffL);
       else if (wave == 1) load_lds4_s(deltab + ld_row, 4 * lane, dst - wdst + C::kOffD);
     } else {
       // a head's last tile: rows past Nq are clamped to Nq - 1
@@ -160,7 +161,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
         load_lds16_s(os, off, dst + C::kOffO + u * kRound);
       }
       const uint32_t loff = 4 * min(lane, last);
-      if (wave == 0) load_lds4_s(lseb + ld_row, loff, dst - wdst + C::kOffL);
+      if (wave == 0) load_lds4_s(nlb + ld_row, loff, dst - wdst + C::kOffL);
       else if (wave == 1) load_lds4_s(deltab + ld_row, loff, dst - wdst + C::kOffD);
     }
     ld_r += C::kBQ;
@@ -283,7 +284,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
 
   bf16x8 abuf[kM1];                 // phase-1 A operands in flight (indexed by product)
   bf16x8 tbuf[kM2];                 // phase-2 A operands in flight
-  f32x4 lbuf[4];                    // lse of 4-query groups rq of the blocks in flight
+  f32x4 lbuf[4];                    // nl of 4-query groups rq of the blocks in flight
   f32x16 dblk;                      // D of the block whose dP products come next
 
   // P and dS of score element e of a block, in two halves of about equal issue cost: the
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
   auto elem_exp = [&](const f32x16& cs, int e) {
     float se = cs[e];
     asm volatile("" : "+v"(se));
-    pe[e] = fast_exp2(__builtin_fmaf(se, c2, lbuf[e >> 2][e & 3] * -kLog2e));
+    pe[e] = fast_exp2(__builtin_fmaf(se, c2, lbuf[e >> 2][e & 3]));
   };
   auto elem_ds = [&](const f32x16& cp, int e, u32x4& pw, u32x4& sw) {
     float dpe = cp[e];                        // D - dP
@@ -308,7 +309,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
 
   // Phase 1 of block j at (st, blk), scores (cs, cp): the S/dP products of block j+1 (at
   // (st_n, blk_n)) into (ns, np), each beside half of one of the score elements 8..15 of block j
-  // (into pf1, sf1).  The last kPf slots start this block's phase-2 reads; lse and D of block j+1's
+  // (into pf1, sf1).  The last kPf slots start this block's phase-2 reads; nl and D of block j+1's
   // first two query groups are read on the way.
   auto phase1 = [&](const f32x16& cs, const f32x16& cp, f32x16& ns, f32x16& np, bf16x8& pf1,
                     bf16x8& sf1, int st, int blk, int st_n, int blk_n) {
@@ -338,7 +339,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
   // Phase 2 of block j at (st, blk): its dV/dK products with (pf, sf), each beside half of one of
   // the score elements 0..7 of block j+1 (scores (ns, np), into pfn0, sfn0), starting two products
   // late so that the S/dP products just issued have finished.  The last kPf slots start the reads
-  // of the next phase 1 (A operands of block j+2 at (st_a, blk_a)); lse and D of block j+1's last
+  // of the next phase 1 (A operands of block j+2 at (st_a, blk_a)); nl and D of block j+1's last
   // two query groups (at (st_n, blk_n)) are read on the way.
   auto phase2 = [&](const bf16x8 (&pf)[2], const bf16x8 (&sf)[2], const f32x16& ns,
                     const f32x16& np, bf16x8& pfn0, bf16x8& sfn0, int st, int blk, int st_n,
@@ -469,7 +470,7 @@ hipError_t launch(const BwdArgs& a) {
   const int64_t nwg = a.BH / a.G * a.R * tpc;
   hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (const __bf16*)a.dout, a.lse, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
+                     (const __bf16*)a.dout, a.nl, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
                      (int)a.H, (int)a.G, a.Nq, a.Nk, (int)a.R, (int)tpc, a.scale * kLog2e,
                      a.scale, a.accumulate_dkv ? 1 : 0);
   return hipGetLastError();

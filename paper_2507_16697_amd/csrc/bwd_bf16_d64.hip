@@ -13,10 +13,11 @@
 // accumulators for its keys in registers.  Per query tile:
 //   S   = Q K^T        A = Q rows (LDS),  B = K rows (LDS)              -> lane = key
 //   dP  = dO V^T       A = dO rows (LDS), B = V rows (LDS)
-//   P   = exp2(S*scale*log2e - lse_i*log2e),  dS = P (dP - D_i)        (fp32)
+//   P   = exp2(S*scale*log2e + nl_i),  dS = P (dP - D_i)                (fp32; nl_i = -lse_i*log2e
+//                                                                      from the preprocess)
 //   dV^T += dO^T P     A = dO^T by transposed LDS reads, B = P from registers
 //   dK^T += Q^T dS     A = Q^T by transposed LDS reads,  B = dS from registers
-// Q, dO, lse and D of the next query tile arrive by direct global->LDS loads while the current
+// Q, dO, nl and D of the next query tile arrive by direct global->LDS loads while the current
 // one is processed (double buffered, one barrier per tile).  K and V tiles are row-major in LDS
 // with XOR-swizzled 16-byte chunks.  The two waves sharing a key block add their dK/dV through
 // LDS at the end.
@@ -47,7 +48,7 @@ struct DkvCfg {
   static constexpr int kOffV = kOffK + kKTile;
   static constexpr int kOffQ = kOffV + kKTile;          // 2 buffers
   static constexpr int kOffO = kOffQ + 2 * kQTile;      // 2 buffers
-  static constexpr int kOffL = kOffO + 2 * kQTile;      // 2 x kBQ floats: lse
+  static constexpr int kOffL = kOffO + 2 * kQTile;      // 2 x kBQ floats: nl
   static constexpr int kOffD = kOffL + 2 * kBQ * 4;     // 2 x kBQ floats: D
   static constexpr int kLds = kOffD + 2 * kBQ * 4;
   static_assert(kQB * 32 * 2 == kBQ, "two query halves");
@@ -90,10 +91,10 @@ __device__ __forceinline__ void issue_rows(const __bf16* __restrict__ src, uint3
   }
 }
 
-// lse and D of queries row0 .. row0 + BQ - 1 (clamped to `last`) into LDS, 4 bytes per lane:
-// waves 0 and 1 load lse, waves 2 and 3 load D.
+// nl and D of queries row0 .. row0 + BQ - 1 (clamped to `last`) into LDS, 4 bytes per lane:
+// waves 0 and 1 load nl, waves 2 and 3 load D.
 template <int BQ>
-__device__ __forceinline__ void issue_rowvals(const float* __restrict__ lseb,
+__device__ __forceinline__ void issue_rowvals(const float* __restrict__ nlb,
                                               const float* __restrict__ deltab, uint32_t ldst,
                                               uint32_t ddst, int64_t row0, int64_t last,
                                               int wave, int lane) {
@@ -103,7 +104,7 @@ __device__ __forceinline__ void issue_rowvals(const float* __restrict__ lseb,
     int64_t r = row0 + part * 64 + lane;
     r = r < last ? r : last;
     if (wave < 2)
-      load_lds4(lseb + r, ldst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
+      load_lds4(nlb + r, ldst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
     else
       load_lds4(deltab + r, ddst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
   }
@@ -112,7 +113,7 @@ __device__ __forceinline__ void issue_rowvals(const float* __restrict__ lseb,
 template <int D>
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
-    const __bf16* __restrict__ dout, const float* __restrict__ lse,
+    const __bf16* __restrict__ dout, const float* __restrict__ nl,
     const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BHkv,
     int H, int grp,
     int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale, int accumulate) {
@@ -147,7 +148,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   const int64_t qh0 = (bh / (H / grp)) * H + (bh % (H / grp)) * grp;
   const __bf16* qb = q + qh0 * Nq * D;
   const __bf16* ob = dout + qh0 * Nq * D;
-  const float* lseb = lse + qh0 * Nq;
+  const float* nlb = nl + qh0 * Nq;
   const float* deltab = delta + qh0 * Nq;
 
   const int64_t nqt = (Nq + C::kBQ - 1) / C::kBQ;
@@ -161,7 +162,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
                 C::kWaves);
   issue_rows<D>(ob, lbase + C::kOffO, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
                 C::kWaves);
-  issue_rowvals<C::kBQ>(lseb, deltab, lbase + C::kOffL, lbase + C::kOffD, 0, Nq - 1, wave, lane);
+  issue_rowvals<C::kBQ>(nlb, deltab, lbase + C::kOffL, lbase + C::kOffD, 0, Nq - 1, wave, lane);
   const float* lds_l = reinterpret_cast<const float*>(lds + C::kOffL);
   const float* lds_d = reinterpret_cast<const float*>(lds + C::kOffD);
 
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   int64_t hn = 0;
   for (int64_t it = 0; it < ntiles; ++it) {
     const int cur = (int)(it & 1);
-    // next query tile in flight: Q, dO rows and their lse, D straight into LDS
+    // next query tile in flight: Q, dO rows and their nl, D straight into LDS
     qn = q0 + C::kBQ;
     if (qn >= Nq) {
       qn = 0;
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
                     C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
       issue_rows<D>(ob + hn * D, lbase + C::kOffO + (cur ^ 1) * C::kQTile, qn, Nq - 1,
                     C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rowvals<C::kBQ>(lseb + hn, deltab + hn, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
+      issue_rowvals<C::kBQ>(nlb + hn, deltab + hn, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
                             lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, qn, Nq - 1, wave, lane);
     }
     // last query tile (rows past Nq are clamped copies) or a partial key tile
@@ -255,7 +256,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
         const int qi = qh * C::kQW + 32 * b + 8 * rq + 4 * g;   // 4 consecutive queries
-        const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + qi) * -kLog2e;
+        const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + qi);
         const f32x4 d4 = *reinterpret_cast<const f32x4*>(cd + qi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -363,7 +364,7 @@ hipError_t launch(const BwdArgs& a) {
   const int64_t nwg = a.BH / a.G * a.R * tpc;
   hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
                      (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (const __bf16*)a.dout, a.lse, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
+                     (const __bf16*)a.dout, a.nl, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
                      (int)a.H, (int)a.G, a.Nq, a.Nk,
                      (int)a.R, (int)tpc, a.scale * kLog2e, a.scale, a.accumulate_dkv ? 1 : 0);
   return hipGetLastError();

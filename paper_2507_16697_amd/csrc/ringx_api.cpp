@@ -199,20 +199,21 @@ ringx_status ringx_lse_merge(const float* part_out, const float* part_lse, void*
 }
 
 
-ringx_status ringx_bwd_preprocess(const void* out, const void* dout, float* delta, int64_t B,
-                                  int64_t H, int64_t Nq, int64_t d, ringx_dtype dtype,
-                                  hipStream_t stream) {
-  if (!out || !dout || !delta) return RINGX_E_NULLPTR;
+ringx_status ringx_bwd_preprocess(const void* out, const void* dout, const float* lse,
+                                  float* delta, int64_t B, int64_t H, int64_t Nq, int64_t d,
+                                  ringx_dtype dtype, hipStream_t stream) {
+  if (!out || !dout || !lse || !delta) return RINGX_E_NULLPTR;
   ringx_status st = check_dims(B, H, Nq, 1, d, 1, 1.0f, dtype);
   if (st != RINGX_OK) return st;
-  for (const void* p : {out, dout, (const void*)delta})
+  for (const void* p : {out, dout, (const void*)lse, (const void*)delta})
     if (!aligned16(p)) return RINGX_E_ALIGN;
   const int64_t es = esize(dtype), bh = B * H;
-  const Span sd = span(delta, bh * Nq * 4);
-  if (overlap(sd, span(out, bh * Nq * d * es)) || overlap(sd, span(dout, bh * Nq * d * es)))
+  const Span sd = span(delta, 2 * bh * Nq * 4);
+  if (overlap(sd, span(out, bh * Nq * d * es)) || overlap(sd, span(dout, bh * Nq * d * es)) ||
+      overlap(sd, span(lse, bh * Nq * 4)))
     return RINGX_E_ALIAS;
   ringx::BwdArgs a;
-  a.out = out, a.dout = dout, a.delta = delta;
+  a.out = out, a.dout = dout, a.lse = lse, a.delta = delta, a.nl = delta + bh * Nq;
   a.BH = bh, a.Nq = Nq, a.Nk = 1, a.d = d, a.R = 1, a.stream = stream, a.H = H, a.G = 1;
   return hip_status(ringx::launch_bwd_pre(a, dtype == RINGX_BF16));
 }
@@ -234,7 +235,7 @@ ringx_status check_bwd_stage(const void* q, const void* k, const void* v, const 
   const int64_t es = esize(dtype), bh = B * H;
   const Span ins[] = {span(q, bh * Nq * d * es), span(k, bh * Nk * d * es),
                       span(v, bh * Nk * d * es), span(dout, bh * Nq * d * es),
-                      span(lse, bh * Nq * 4), span(delta, bh * Nq * 4)};
+                      span(lse, bh * Nq * 4), span(delta, 2 * bh * Nq * 4)};
   for (auto oi = outs.begin(); oi != outs.end(); ++oi) {
     for (const Span& i : ins)
       if (overlap(*oi, i)) return RINGX_E_ALIAS;
@@ -259,7 +260,7 @@ ringx_status ringx_attn_bwd_dkdv(const void* q, const void* k, const void* v, co
   if (st != RINGX_OK) return st;
   ringx::BwdArgs a;
   a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.dk = dk, a.dv = dv;
-  a.delta = const_cast<float*>(delta);
+  a.delta = const_cast<float*>(delta), a.nl = const_cast<float*>(delta) + bh * Nq;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.H = H, a.G = 1;
   a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dkdv_bf16(a)
@@ -277,7 +278,7 @@ ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, cons
   if (st != RINGX_OK) return st;
   ringx::BwdArgs a;
   a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.dq = dq;
-  a.delta = const_cast<float*>(delta);
+  a.delta = const_cast<float*>(delta), a.nl = const_cast<float*>(delta) + bh * Nq;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale, a.stream = stream;
   a.H = H, a.G = 1;
   return hip_status(dtype == RINGX_BF16 ? ringx::launch_bwd_dq_bf16(a)
@@ -287,8 +288,8 @@ ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, cons
 size_t ringx_bwd_workspace_bytes(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d,
                                  int64_t R, ringx_dtype dtype) {
   if (check_dims(B, H, Nq, Nk, d, R, 1.0f, dtype) != RINGX_OK) return 0;
-  const int64_t delta = B * H * Nq * 4;
-  return static_cast<size_t>((delta + 255) / 256 * 256);
+  const int64_t stats = 2 * B * H * Nq * 4;   // D and nl of every query row
+  return static_cast<size_t>((stats + 255) / 256 * 256);
 }
 
 }  // extern "C"
@@ -324,7 +325,7 @@ ringx_status bwd_impl(const void* q, const void* k, const void* v, const void* o
   float* delta = static_cast<float*>(workspace);
   ringx::BwdArgs a;
   a.q = q, a.k = k, a.v = v, a.out = out, a.dout = dout, a.lse = lse;
-  a.dq = dq, a.dk = dk, a.dv = dv, a.delta = delta;
+  a.dq = dq, a.dk = dk, a.dv = dv, a.delta = delta, a.nl = delta + bh * Nq;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale;
   a.H = H, a.G = H / Hkv;
   a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
@@ -397,6 +398,7 @@ ringx_status ringx_attn_bwd_step(const void* q, const void* k, const void* v, co
   if (st != RINGX_OK) return st;
   ringx::BwdArgs a;
   a.q = q, a.k = k, a.v = v, a.dout = dout, a.lse = lse, a.delta = const_cast<float*>(delta);
+  a.nl = const_cast<float*>(delta) + bh * Nq;
   a.dq = dq_acc, a.dk = dk, a.dv = dv;
   a.BH = bh, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = 1, a.scale = scale, a.H = H, a.G = 1;
   a.accumulate_dkv = accumulate_dkv != 0, a.accumulate_dq = accumulate_dq != 0, a.stream = stream;
@@ -450,15 +452,16 @@ ringx_status ringx_tt_tokenize(const float* field, void* tokens, int64_t C, int6
 }  // extern "C"
 
 // ------------------------------------------------------------------------------------------------
-// ringx_attn_bwd_noalloc: ringx_attn_bwd with D (one fp32 per query row) in a fixed, file-scope
-// device array instead of a caller workspace.  Every GPU the library runs on holds its own copy of
-// the array (RINGX_NOALLOC_MAX_ROWS * 4 bytes = 8 MiB) until the process ends.  In host code the
+// ringx_attn_bwd_noalloc: ringx_attn_bwd with its per-row statistics (D and nl, two fp32 per query
+// row) in a fixed, file-scope device array instead of a caller workspace.  Every GPU the library
+// runs on holds its own copy of the array (RINGX_NOALLOC_MAX_ROWS * 8 bytes = 16 MiB) until the
+// process ends.  In host code the
 // array's name is only a host-side stand-in: its device address is looked up once per device with
 // hipGetSymbolAddress (with that device current) and only that address is ever passed to kernels.
 
 namespace {
 
-__device__ __align__(256) float scratch[RINGX_NOALLOC_MAX_ROWS];
+__device__ __align__(256) float scratch[2 * RINGX_NOALLOC_MAX_ROWS];
 
 constexpr int kMaxDevices = 64;
 std::mutex g_scratch_mu;
@@ -504,7 +507,7 @@ ringx_status ringx_attn_bwd_noalloc(const void* q, const void* k, const void* v,
   if (st != RINGX_OK) return st;
   static_assert(RINGX_NOALLOC_MAX_ROWS % 64 == 0, "whole 256-byte blocks");
   return bwd_impl(q, k, v, out, dout, lse, dq, dk, dv, B, H, H, Nq, Nk, d, R, scale, dtype,
-                  accumulate_dkv, ws, sizeof(float) * (size_t)RINGX_NOALLOC_MAX_ROWS, stream);
+                  accumulate_dkv, ws, sizeof(float) * 2 * (size_t)RINGX_NOALLOC_MAX_ROWS, stream);
 }
 
 }  // extern "C"

@@ -52,6 +52,7 @@ struct BwdArgs {
   float* dk = nullptr;
   float* dv = nullptr;
   float* delta = nullptr;       // D_i = dout_i . out_i, [B,H,Nq]
+  float* nl = nullptr;          // -lse_i * log2(e), [B,H,Nq] (the exponent's offset, base 2)
   int64_t BH = 0, Nq = 0, Nk = 0, d = 0, R = 1;   // BH = B * H query heads
   int64_t H = 1, G = 1;         // query heads per batch; query heads per K/V head (GQA)
   float scale = 1.f;

@@ -109,7 +109,7 @@ def ring_backward(q, k_chunks, v_chunks, out, dout, lse, scale=None, overlap=Tru
     B, H, Nq, d = q.shape
     compute = torch.cuda.current_stream()
     copy, pp = _start(torch, compute, overlap, k_chunks[0], max(k.shape[2] for k in k_chunks))
-    delta = ringx.ringx_bwd_preprocess(out, dout, stream=compute)
+    delta = ringx.ringx_bwd_preprocess(out, dout, lse, stream=compute)
     dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=q.device)
     dks = [torch.empty(k.shape, dtype=torch.float32, device=q.device) for k in k_chunks]
     dvs = [torch.empty_like(t) for t in dks]

@@ -73,7 +73,7 @@ def lib() -> ctypes.CDLL:
         L.ringx_attn_bwd_noalloc.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I,
                                              _I, _I, ctypes.c_float, ctypes.c_int, ctypes.c_int,
                                              _P]
-        L.ringx_bwd_preprocess.argtypes = [_P, _P, _P, _I, _I, _I, _I, ctypes.c_int, _P]
+        L.ringx_bwd_preprocess.argtypes = [_P, _P, _P, _P, _I, _I, _I, _I, ctypes.c_int, _P]
         L.ringx_attn_bwd_dkdv.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
                                           ctypes.c_float, ctypes.c_int, ctypes.c_int, _P]
         L.ringx_attn_bwd_dq.argtypes = [_P, _P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I,
@@ -181,7 +181,7 @@ def _check_grad_inputs(q, dout, lse, delta):
     B, H, Nq, _ = q.shape
     _expect("dout", dout, q.shape, q.dtype, q.device)
     _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
-    _expect("delta", delta, (B, H, Nq), torch.float32, q.device)
+    _expect("delta", delta, (2, B, H, Nq), torch.float32, q.device)
 
 
 def _stream(stream):
@@ -318,21 +318,24 @@ def ringx_attn_bwd_noalloc(q, k, v, out, dout, lse, R: int, dq, dk, dv, scale=No
     return dq, dk, dv
 
 
-def ringx_bwd_preprocess(out, dout, delta=None, stream=None):
-    """delta [B,H,Nq] fp32 = rowsum(dout * out)."""
+def ringx_bwd_preprocess(out, dout, lse, delta=None, stream=None):
+    """Per-row statistics delta [2,B,H,Nq] fp32: delta[0] = rowsum(dout * out),
+    delta[1] = -lse * log2(e)."""
     torch = _torch()
-    _dev(out, dout)
+    _dev(out, dout, lse)
     if out.dim() != 4:
         raise ValueError("out must be 4-D [B, H, Nq, d]")
     _dtype_code(out)
     B, H, Nq, d = out.shape
     _expect("dout", dout, out.shape, out.dtype, out.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, out.device)
     if delta is None:
-        delta = torch.empty((B, H, Nq), dtype=torch.float32, device=out.device)
+        delta = torch.empty((2, B, H, Nq), dtype=torch.float32, device=out.device)
     _dev(delta)
-    _expect("delta", delta, (B, H, Nq), torch.float32, out.device)
-    st = lib().ringx_bwd_preprocess(out.data_ptr(), dout.data_ptr(), delta.data_ptr(), B, H, Nq,
-                                    d, _dtype_code(out), _stream(stream))
+    _expect("delta", delta, (2, B, H, Nq), torch.float32, out.device)
+    st = lib().ringx_bwd_preprocess(out.data_ptr(), dout.data_ptr(), lse.data_ptr(),
+                                    delta.data_ptr(), B, H, Nq, d, _dtype_code(out),
+                                    _stream(stream))
     _check("ringx_bwd_preprocess", st)
     return delta
 

@@ -152,15 +152,17 @@ def test_backward_noalloc_validation():
     assert bwd_noalloc(B=3, H=5, Nq=1 << 20) == SCRATCH
 
 
-def pre(o=QP, do=KP, dl=LP, B=1, H=2, Nq=100, d=64, dt=BF16):
-    return ringx.lib().ringx_bwd_preprocess(o, do, dl, B, H, Nq, d, dt, None)
+def pre(o=QP, do=KP, l=VP, dl=LP, B=1, H=2, Nq=100, d=64, dt=BF16):
+    return ringx.lib().ringx_bwd_preprocess(o, do, l, dl, B, H, Nq, d, dt, None)
 
 
 def test_preprocess_validation():
-    assert pre(o=0) == NULLPTR and pre(dl=0) == NULLPTR
+    assert pre(o=0) == NULLPTR and pre(l=0) == NULLPTR and pre(dl=0) == NULLPTR
     assert pre(B=0) == SHAPE and pre(d=96) == UNSUP
-    assert pre(dl=LP + 4) == ALIGN
-    assert pre(dl=QP) == ALIAS
+    assert pre(dl=LP + 4) == ALIGN and pre(l=VP + 8) == ALIGN
+    assert pre(dl=QP) == ALIAS and pre(dl=VP) == ALIAS
+    # delta holds two rows of B*H*Nq floats (D, then nl): lse just past the first row overlaps it
+    assert pre(l=LP + 800) == ALIAS
 
 
 def dkdv(dk=OP, dv=OP + 8 * GB, lse=LP, delta=LP + 8 * GB, R=3, d=64, acc=0):
@@ -180,6 +182,7 @@ def test_gradient_stage_validation():
     assert dkdv(dv=OP + 8 * GB + 4) == ALIGN and dqs(dq=OP + 8) == ALIGN
     assert dkdv(dv=OP) == ALIAS and dkdv(dk=KP) == ALIAS and dqs(dq=LP) == ALIAS
     assert dqs(dq=LP + 8 * GB) == ALIAS    # dq over delta
+    assert dqs(dq=LP + 8 * GB + 800) == ALIAS    # dq over delta's second row (nl)
 
 
 def fstep(q=QP, k=KP, v=VP, o=OP, l=LP, B=1, H=2, Nq=100, Nk=300, d=64, scale=0.125, dt=BF16,

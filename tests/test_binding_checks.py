@@ -47,13 +47,16 @@ def test_expect():
 def test_gradient_inputs():
     q = _t(1, 2, 10, 64)
     lse = _t(1, 2, 10, dtype=torch.float32)
-    ringx._check_grad_inputs(q, _t(1, 2, 10, 64), lse, lse)
+    delta = _t(2, 1, 2, 10, dtype=torch.float32)
+    ringx._check_grad_inputs(q, _t(1, 2, 10, 64), lse, delta)
     with pytest.raises(ValueError, match="dout: shape"):
-        ringx._check_grad_inputs(q, _t(1, 2, 11, 64), lse, lse)
+        ringx._check_grad_inputs(q, _t(1, 2, 11, 64), lse, delta)
     with pytest.raises(ValueError, match="delta: shape"):
-        ringx._check_grad_inputs(q, _t(1, 2, 10, 64), lse, _t(1, 2, 9, dtype=torch.float32))
+        ringx._check_grad_inputs(q, _t(1, 2, 10, 64), lse, _t(2, 1, 2, 9, dtype=torch.float32))
+    with pytest.raises(ValueError, match="delta: shape"):
+        ringx._check_grad_inputs(q, _t(1, 2, 10, 64), lse, lse)
     with pytest.raises(TypeError, match="lse: dtype"):
-        ringx._check_grad_inputs(q, _t(1, 2, 10, 64), _t(1, 2, 10), lse)
+        ringx._check_grad_inputs(q, _t(1, 2, 10, 64), _t(1, 2, 10), delta)
 
 
 def test_wrappers_refuse_host_tensors():

@@ -316,13 +316,16 @@ def test_backward_stages_compose(dtype, d):
     scale = float(np.float32(1 / math.sqrt(d)))
     out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
     dq, dk, dv = ringx.ringx_attn_bwd(g["q"], g["k"], g["v"], out, g["do"], lse, R, scale=scale)
-    delta = ringx.ringx_bwd_preprocess(out, g["do"])
+    delta = ringx.ringx_bwd_preprocess(out, g["do"], lse)
     dk2, dv2 = ringx.ringx_attn_bwd_dkdv(g["q"], g["k"], g["v"], g["do"], lse, delta, R, scale=scale)
     dq2 = ringx.ringx_attn_bwd_dq(g["q"], g["k"], g["v"], g["do"], lse, delta, R, scale=scale)
     torch.cuda.synchronize()
     assert torch.equal(dq, dq2) and torch.equal(dk, dk2) and torch.equal(dv, dv2)
     ref_d = (to_host_f64(out) * x["do"]).sum(axis=-1)
-    assert max_abs_err(to_host_f64(delta), ref_d) <= 1e-4 * max(1.0, float(np.abs(ref_d).max()))
+    assert max_abs_err(to_host_f64(delta[0]), ref_d) <= 1e-4 * max(1.0, float(np.abs(ref_d).max()))
+    # the second row: the lse in the base-2 exponent form, -lse * log2(e), to fp32 rounding
+    ref_nl = -to_host_f64(lse) / math.log(2.0)
+    assert max_abs_err(to_host_f64(delta[1]), ref_nl) <= 2.0 ** -22 * max(1.0, float(np.abs(ref_nl).max()))
 
 
 def test_errors_leave_outputs_untouched():
@@ -360,9 +363,9 @@ def test_mismatched_buffers_are_refused_before_launch():
         ringx.ringx_attn_bwd(q, k, v, out, do, lse, 2, dk=torch.zeros((1, 2, 40, 64), **bf))
     with pytest.raises(ValueError, match="dv: shape"):
         ringx.ringx_attn_bwd(q, k, v, out, do, lse, 2, dv=torch.zeros((1, 2, 39, 64), **f32))
-    delta = torch.zeros((1, 2, 16), **f32)
+    delta = torch.zeros((2, 1, 2, 16), **f32)
     with pytest.raises(ValueError, match="delta: shape"):
-        ringx.ringx_attn_bwd_dq(q, k, v, do, lse, delta[:, :, :8].contiguous(), 2)
+        ringx.ringx_attn_bwd_dq(q, k, v, do, lse, delta[0].contiguous(), 2)
     with pytest.raises(TypeError, match="out_acc: dtype"):
         ringx.ringx_attn_fwd_step(q, k, v, torch.zeros((1, 2, 16, 64), **bf), lse, True)
     with pytest.raises(ValueError, match="dk: shape"):

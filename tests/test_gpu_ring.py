@@ -115,7 +115,7 @@ def test_bwd_step_accumulate_dkv():
     t, _ = random_case(46, B, H, Nq, Nk, d, store="bf16", std=2 ** -0.5)
     g = {k: to_device(v, "bf16") for k, v in t.items()}
     out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], 1)
-    delta = ringx.ringx_bwd_preprocess(out, g["do"])
+    delta = ringx.ringx_bwd_preprocess(out, g["do"], lse)
     f32 = dict(dtype=torch.float32, device="cuda")
     dq, dk, dv = torch.empty((B, H, Nq, d), **f32), torch.empty((B, H, Nk, d), **f32), \
         torch.empty((B, H, Nk, d), **f32)

@@ -116,9 +116,9 @@ def test_backward_entry_points(store, d):
     f32 = torch.float32
     out, lse = ringx.ringx_attn_fwd(q, k, v, R)
 
-    ref_delta = ringx.ringx_bwd_preprocess(out, do)
-    delta = Guarded((B, H, Nq), f32)
-    ringx.ringx_bwd_preprocess(out, do, delta=delta.t)
+    ref_delta = ringx.ringx_bwd_preprocess(out, do, lse)
+    delta = Guarded((2, B, H, Nq), f32)
+    ringx.ringx_bwd_preprocess(out, do, lse, delta=delta.t)
     delta.check("delta")
     _same("delta", delta.t, ref_delta)
 

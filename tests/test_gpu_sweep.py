@@ -198,7 +198,7 @@ def test_sweep_ring_backward(case):
     i, store, B, hkv, grp, nq, nk, d, R = case
     x, g, scale = _inputs(case)
     out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], R, scale=scale)
-    delta = ringx.ringx_bwd_preprocess(out, g["do"])
+    delta = ringx.ringx_bwd_preprocess(out, g["do"], lse)
     dq = torch.empty((B, hkv, nq, d), dtype=torch.float32, device="cuda")
     dk = torch.empty((B, hkv, nk, d), dtype=torch.float32, device="cuda")
     dv = torch.empty_like(dk)

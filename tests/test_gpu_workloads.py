@@ -36,7 +36,7 @@ def _run(w, g, with_bwd=True):
     out, lse = ringx.ringx_attn_fwd(g["q"], g["k"], g["v"], w.R, scale=w.scale)
     res = {"out": out, "lse": lse}
     if with_bwd:
-        delta = ringx.ringx_bwd_preprocess(out, g["do"])
+        delta = ringx.ringx_bwd_preprocess(out, g["do"], lse)
         res["dk"], res["dv"] = ringx.ringx_attn_bwd_dkdv(g["q"], g["k"], g["v"], g["do"], lse,
                                                          delta, w.R, scale=w.scale)
         res["dq"] = ringx.ringx_attn_bwd_dq(g["q"], g["k"], g["v"], g["do"], lse, delta, w.R,
