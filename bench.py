@@ -156,8 +156,9 @@ def input_sha256(t):
 class ClockSampler:
     """Samples the GPU's shader clock (rocm-smi) on a host thread while the timed steps run."""
 
-    def __init__(self, period=0.5):
+    def __init__(self, period=0.5, enabled=True):
         import threading
+        self.enabled = enabled
         self.period = period
         self.samples = []
         self.error = None
@@ -188,12 +189,16 @@ class ClockSampler:
             self._stop.wait(self.period)
 
     def __enter__(self):
-        self._thread.start()
+        if self.enabled:
+            self._thread.start()
+        else:
+            self.error = "not sampled (--no-sclk)"
         return self
 
     def __exit__(self, *exc):
         self._stop.set()
-        self._thread.join(timeout=15)
+        if self.enabled:
+            self._thread.join(timeout=15)
 
     def record(self):
         if not self.samples:
@@ -332,6 +337,223 @@ def other_shapes(torch, np, inputs, ringx, stream, dev):
     return res
 
 
+# ------------------------------------------------------------------------------------------------
+# rocprofv3 outputs -> profiles/ summaries (CPU only; the commands that make the outputs are written
+# into each summary)
+
+PROFILE_STEP = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ring --no-gqa "
+                "--no-tokenizer --no-shapes --no-sclk")
+PROFILE_TRACE = ("python -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-ring --no-gqa "
+                 "--no-tokenizer --no-shapes --no-sclk")
+BUSY_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CYCLES "
+                 "SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS GRBM_GUI_ACTIVE")
+
+# mangled-name fragment -> (label in the summaries, traffic key, source files of its hash)
+PROFILE_KERNELS = [
+    ("fwd_bf16_kernelILi128ELi0E", "fwd_bf16_kernel<128, fused merge>", "fwd_bf16",
+     ["fwd_bf16.hip", "ringx_device.h"]),
+    ("fwd_bf16_kernelILi128ELi1E", "fwd_bf16_kernel<128, partials>", "fwd_bf16_partials",
+     ["fwd_bf16.hip", "ringx_device.h"]),
+    ("bwd_dkdv_kernelILi128E", "bwd_dkdv_kernel<128>", "bwd_dkdv", ["bwd_bf16.hip", "ringx_device.h"]),
+    ("bwd_dq_kernelILi128E", "bwd_dq_kernel<128>", "bwd_dq", ["bwd_dq_bf16.hip", "ringx_device.h"]),
+    ("bwd_pre_bf16_kernelILi128E", "bwd_pre_bf16_kernel<128>", "bwd_pre", ["bwd_pre.hip", "ringx_device.h"]),
+    ("merge_vec4_kernelILb1E", "merge_vec4_kernel<bf16 out>", "lse_merge", ["merge.hip", "ringx_device.h"]),
+]
+
+
+def _profile_kernel(name):
+    """rocprofv3 prints some names mangled and some demangled: match either form."""
+    demangled = {"ILi128ELi0E": "<128, 0>", "ILi128ELi1E": "<128, 1>", "ILi128E": "<128>",
+                 "ILb1E": "<true>"}
+    for frag, label, key, files in PROFILE_KERNELS:
+        if frag in name:
+            return label, key, files
+        for m, dm in demangled.items():
+            if frag.endswith(m) and frag[: -len(m)] + dm in name.replace("(anonymous namespace)::", ""):
+                return label, key, files
+    return None
+
+
+def _read_csv(path):
+    import csv
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _pmc_per_dispatch(dirpath, counter):
+    """{dispatch id: (kernel name, value)} of one counter from a rocprofv3 --pmc CSV."""
+    rows = _read_csv(os.path.join(dirpath, "pmc_counter_collection.csv"))
+    out = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        did = int(r["Dispatch_Id"])
+        name, val = out.get(did, (r["Kernel_Name"], 0.0))
+        out[did] = (name, val + float(r["Counter_Value"]))
+    return out
+
+
+def summarize_profiles(root, workload):
+    from paper_2507_16697_amd import inputs
+    w = inputs.WORKLOADS[workload]
+    B, H, Nq, Nk, d, R = w.B, w.H, w.Nq, w.Nk, w.d, w.R
+    rows = B * H * Nq
+    shape = f"B={B}, H={H}, Nq={Nq}, Nk={Nk}, d={d}, R={R}, bf16"
+    prof = os.path.join(ROOT, "profiles")
+    cmd = lambda d_, o, extra: f"rocprofv3 {extra} --output-format csv -d gpurun_out/{d_} -o {o} -- "
+
+    # kernel trace
+    stats = _read_csv(os.path.join(root, "prof_trace", "ring8_kernel_stats.csv"))
+    lines = []
+    for r in stats:
+        k = _profile_kernel(r["Name"])
+        if k:
+            lines.append((k[0], int(r["Calls"]), float(r["AverageNs"]), float(r["MinNs"]),
+                          float(r["MaxNs"])))
+    lines.sort(key=lambda x: -x[2])
+    bench_line = None
+    log_path = os.path.join(root, "prof_trace.log")
+    if os.path.exists(log_path):
+        for line in open(log_path):
+            if line.startswith("{") and '"metric"' in line:
+                bench_line = json.loads(line)
+    md = [f"# Kernel trace: {workload} ({shape})", "",
+          "Command (run from the repository root on one MI355X):", "",
+          "    " + cmd("prof_trace", "ring8", "--kernel-trace --stats") + PROFILE_TRACE, "",
+          "The run makes 4 forward and 4 backward passes (1 warmup + 3 timed; each backward = "
+          "preprocess + dK/dV + dQ), 1 partials forward and 11 standalone merges.  Durations in ns; "
+          "only libringx kernels are listed.", "",
+          "| kernel | calls | average ns | min ns | max ns |", "|---|---|---|---|---|"]
+    md += [f"| {a} | {c} | {avg:.0f} | {mn:.0f} | {mx:.0f} |" for a, c, avg, mn, mx in lines]
+    if bench_line:
+        c = bench_line["config"]
+        md += ["", f"bench.py in the same run (HIP events around each call, "
+               f"{bench_line['steps']} timed steps): step {bench_line['ms_per_step']:.2f} ms = fwd "
+               f"{c['fwd_ms']:.2f} + preprocess {c['bwd_pre_ms']:.3f} + dK/dV {c['bwd_dkdv_ms']:.2f} "
+               f"+ dQ {c['bwd_dq_ms']:.2f} ms; {bench_line['value']:.1f} TFLOP/s "
+               f"(12*B*H*Nq*Nk*d per step) = {100 * bench_line['value'] / PEAK_BF16_TFLOPS:.2f}% of "
+               f"{PEAK_BF16_TFLOPS}."]
+    with open(os.path.join(prof, f"kernel_trace_{workload}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+
+    # HBM traffic: FETCH_SIZE / WRITE_SIZE per dispatch, calibrated on the 1 GiB copy
+    fetch = _pmc_per_dispatch(os.path.join(root, "pmc_FETCH_SIZE"), "FETCH_SIZE")
+    write = _pmc_per_dispatch(os.path.join(root, "pmc_WRITE_SIZE"), "WRITE_SIZE")
+    cf = _pmc_per_dispatch(os.path.join(root, "pmc_copy_FETCH_SIZE"), "FETCH_SIZE")
+    cw = _pmc_per_dispatch(os.path.join(root, "pmc_copy_WRITE_SIZE"), "WRITE_SIZE")
+    copy_bytes = 1 << 30
+    cf_kib = sorted(v for _, v in cf.values())[len(cf) // 2]
+    cw_kib = sorted(v for _, v in cw.values())[len(cw) // 2]
+    ff, wf = copy_bytes / (cf_kib * 1024), copy_bytes / (cw_kib * 1024)
+    es = 2
+    alg = {
+        "fwd_bf16": rows * d * es + 2 * B * H * Nk * d * es + rows * d * es + rows * 4,
+        "fwd_bf16_partials": rows * d * es + 2 * B * H * Nk * d * es + R * rows * (4 * d + 4),
+        "bwd_dkdv": 2 * B * H * Nk * d * es + 2 * rows * d * es + 2 * rows * 4
+        + 2 * B * H * Nk * d * 4,
+        "bwd_dq": 2 * B * H * Nk * d * es + 2 * rows * d * es + 2 * rows * 4 + rows * d * 4,
+        "bwd_pre": 2 * rows * d * es + rows * 4 + 2 * rows * 4,
+        "lse_merge": R * rows * (4 * d + 4) + rows * (d * es + 4),
+    }
+    per_kernel = {}
+    for src, which in ((fetch, 0), (write, 1)):
+        for did, (name, val) in src.items():
+            k = _profile_kernel(name)
+            if k:
+                per_kernel.setdefault(k[1], ([], [], k[2]))[which].append(val)
+    cmds = [cmd("pmc_FETCH_SIZE", "pmc", "--pmc FETCH_SIZE") + PROFILE_STEP,
+            cmd("pmc_WRITE_SIZE", "pmc", "--pmc WRITE_SIZE") + PROFILE_STEP,
+            cmd("pmc_copy_FETCH_SIZE", "pmc", "--pmc FETCH_SIZE") + "python -u bench.py --copy-probe",
+            cmd("pmc_copy_WRITE_SIZE", "pmc", "--pmc WRITE_SIZE") + "python -u bench.py --copy-probe"]
+    md = [f"# HBM traffic per launch: {workload} ({shape})", "",
+          "Counters: `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch, L2-to-fabric traffic, so reads "
+          "served by", "the MALL count as fetched), each in a run of its own:", ""]
+    md += ["    " + c for c in cmds[:2]]
+    md += ["", "Calibration: the same counters on a plain 1 GiB device copy (`bench.py --copy-probe`, "
+           "3 copies):", ""] + ["    " + c for c in cmds[2:]]
+    md += ["", f"The copy reads 1 GiB and writes 1 GiB; FETCH_SIZE reports {cf_kib:.0f} KiB and "
+           f"WRITE_SIZE {cw_kib:.0f} KiB, so fetched bytes = FETCH_SIZE x 1024 x {ff:.4f} and written "
+           f"bytes = WRITE_SIZE x 1024 x {wf:.4f}.", "",
+           "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | fetched GB | written GB | traffic GB | "
+           "algorithmic GB | traffic / algorithmic |", "|---|---|---|---|---|---|---|---|"]
+    for key in ("fwd_bf16", "fwd_bf16_partials", "bwd_dkdv", "bwd_dq", "bwd_pre", "lse_merge"):
+        if key not in per_kernel:
+            continue
+        fv, wv, files = per_kernel[key]
+        fk = sorted(fv)[len(fv) // 2]
+        wk = sorted(wv)[len(wv) // 2] if wv else 0.0
+        fb, wb = fk * 1024 * ff, wk * 1024 * wf
+        md.append(f"| {key} | {fk:.0f} | {wk:.0f} | {fb / 1e9:.3f} | {wb / 1e9:.3f} | "
+                  f"{(fb + wb) / 1e9:.3f} | {alg[key] / 1e9:.3f} | {(fb + wb) / alg[key]:.2f} |")
+        rec = {"kernel": key, "workload": workload, "source_hash": kernel_source_hash(files),
+               "fetch_size_kib": fk, "write_size_kib": wk, "fetch_factor": ff, "write_factor": wf,
+               "bytes_fetched": fb, "bytes_written": wb, "bytes_per_launch": fb + wb,
+               "algorithmic_bytes": alg[key], "commands": cmds}
+        with open(os.path.join(prof, f"traffic_{key}_{workload}.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+    md += ["", "Algorithmic bytes: every input read once and every output written once (fwd: Q, K, "
+           "V, out, lse;", "dK/dV: K, V, Q, dO, nl, D, fp32 dK and dV; dQ: K, V, Q, dO, lse, D, fp32 "
+           "dQ; preprocess: out, dout, lse,", "D and nl; merge: R fp32 partials and lse, bf16 out and "
+           "lse).  Traffic well above it is re-reading", "of K/V (forward, dQ) or Q/dO (dK/dV) that "
+           "missed L2."]
+    with open(os.path.join(prof, f"hbm_traffic_{workload}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+
+    # matrix-core, vector and LDS activity from one counter pass
+    busy_rows = _read_csv(os.path.join(root, "pmc_busy", "pmc_counter_collection.csv"))
+    disp = {}
+    for r in busy_rows:
+        did = int(r["Dispatch_Id"])
+        e = disp.setdefault(did, {"name": r["Kernel_Name"], "t0": int(r["Start_Timestamp"]),
+                                  "t1": int(r["End_Timestamp"])})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    md = [f"# Matrix-core and LDS activity: {workload} ({shape})", "",
+          "Command (run from the repository root on one MI355X, one counter pass):", "",
+          "    " + cmd("pmc_busy", "pmc", "--pmc " + BUSY_COUNTERS) + PROFILE_STEP, "",
+          "GRBM_GUI_ACTIVE counts GPU clocks summed over the 8 XCDs, so cycles = GRBM_GUI_ACTIVE / 8 "
+          "and the", "average shader clock = cycles / kernel duration.  MFMA busy = "
+          "SQ_VALU_MFMA_BUSY_CYCLES / (cycles x 1024", "SIMDs); MFMA co-issue = "
+          "SQ_VALU_MFMA_COEXEC_CYCLES / SQ_VALU_MFMA_BUSY_CYCLES (matrix-core cycles during", "which "
+          "the vector ALU also issued); LDS busy = SQ_LDS_IDX_ACTIVE / (cycles x 256 CUs).  The bf16 "
+          "rate the", "matrix cores deliver is MFMA busy x clock / 2.4 GHz x 2516.6 TFLOP/s.", "",
+          "| kernel | duration ms | clock GHz | MFMA busy | MFMA co-issue | delivered TFLOP/s | LDS "
+          "busy | LDS bank conflicts | LDS instructions |", "|---|---|---|---|---|---|---|---|---|"]
+    seen = set()
+    for did in sorted(disp):
+        e = disp[did]
+        k = _profile_kernel(e["name"])
+        if not k or k[0] in seen:
+            continue
+        seen.add(k[0])
+        ms = (e["t1"] - e["t0"]) * 1e-6
+        cyc = e.get("GRBM_GUI_ACTIVE", 0.0) / 8
+        ghz = cyc / (ms * 1e6) if ms > 0 else 0.0
+        busy = e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (cyc * 1024) if cyc else 0.0
+        co = (e.get("SQ_VALU_MFMA_COEXEC_CYCLES", 0.0) / e["SQ_VALU_MFMA_BUSY_CYCLES"]
+              if e.get("SQ_VALU_MFMA_BUSY_CYCLES") else 0.0)
+        lds = e.get("SQ_LDS_IDX_ACTIVE", 0.0) / (cyc * 256) if cyc else 0.0
+        md.append(f"| {k[0]} | {ms:.2f} | {ghz:.2f} | {100 * busy:.1f}% | {100 * co:.1f}% | "
+                  f"{busy * ghz / 2.4 * PEAK_BF16_TFLOPS:.0f} | {100 * lds:.1f}% | "
+                  f"{e.get('SQ_LDS_BANK_CONFLICT', 0.0):.0f} | {e.get('SQ_INSTS_LDS', 0.0):.3e} |")
+    md += ["", "Delivered TFLOP/s counts every executed product (the forward 2U, dK/dV 4U with S "
+           "recomputed, dQ 3U", "with S and dP recomputed), so it exceeds the credited rates of "
+           "bench.py for the two backward kernels."]
+    with open(os.path.join(prof, f"mfma_busy_{workload}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
+    # the bench line of a plain `python bench.py` run beside the profiles, if there is one
+    full = os.path.join(root, "bench.json")
+    if os.path.exists(full):
+        for line in open(full):
+            if line.startswith("{") and '"metric"' in line:
+                bench_line = json.loads(line)
+    if bench_line:
+        with open(os.path.join(prof, f"bench_{workload}.json"), "w") as f:
+            json.dump(bench_line, f, indent=1)
+            f.write("\n")
+    print(f"wrote summaries of {root} under profiles/")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -355,7 +577,18 @@ def main():
                          "tokens, 524k long step)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (calibrates HBM byte counters)")
+    ap.add_argument("--no-sclk", action="store_true",
+                    help="do not sample the shader clock with rocm-smi (for runs under rocprofv3, "
+                         "whose preloaded library would make the tool's own launcher initialise "
+                         "the GPU)")
+    ap.add_argument("--profile-summary", metavar="DIR",
+                    help="CPU only: turn the rocprofv3 outputs under DIR (prof_trace, pmc_FETCH_SIZE, "
+                         "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE, pmc_busy) into "
+                         "the summaries under profiles/")
     args = ap.parse_args()
+    if args.profile_summary:
+        summarize_profiles(args.profile_summary, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU's share of the ring; --gpus {args.gpus} is not supported "
               "(this build has no multi-GPU path)", file=sys.stderr)
@@ -430,7 +663,7 @@ def main():
     K = args.steps
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     torch.cuda.synchronize()
-    with ClockSampler() as clock:
+    with ClockSampler(enabled=not args.no_sclk) as clock:
         wall0 = time.perf_counter()
         for s_ in range(K):
             step(ev[s_])
@@ -473,8 +706,9 @@ def main():
                           "tflops": tf(U, dq_ms),
                           "traffic": load_traffic("bwd_dq", w.name,
                                                   kernel_source_hash(["bwd_dq_bf16.hip", "ringx_device.h"]))},
-        "bwd_pre_bf16_kernel": {"ms": pre_ms, "bytes": B * H * Nq * (4 * d + 4),
-                                "GB/s": B * H * Nq * (4 * d + 4) / (pre_ms * 1e-3) / 1e9},
+        # reads out, dout (bf16) and lse; writes D and nl
+        "bwd_pre_bf16_kernel": {"ms": pre_ms, "bytes": B * H * Nq * (4 * d + 12),
+                                "GB/s": B * H * Nq * (4 * d + 12) / (pre_ms * 1e-3) / 1e9},
     }
     # executed products (the recomputed S and dP included): what the matrix cores actually ran
     for name, units in (("fwd_bf16_kernel", 2), ("bwd_dkdv_kernel", 4), ("bwd_dq_kernel", 3)):
