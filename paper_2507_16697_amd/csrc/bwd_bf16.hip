@@ -117,10 +117,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
 
   // the grp query heads sharing this K/V head are swept one after the other
   const int64_t qh0 = (bh / (H / grp)) * H + (bh % (H / grp)) * grp;
-  const char* qb = reinterpret_cast<const char*>(q + qh0 * Nq * D);
-  const char* ob = reinterpret_cast<const char*>(dout + qh0 * Nq * D);
-  const float* nlb = nl + qh0 * Nq;
-  const float* deltab = delta + qh0 * Nq;
+  // wave-uniform bases in SGPRs, so that the per-tile load addresses are scalar arithmetic
+  const char* qb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(q + qh0 * Nq * D)));
+  const char* ob =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(dout + qh0 * Nq * D)));
+  const float* nlb = static_cast<const float*>(uniform_ptr(nl + qh0 * Nq));
+  const float* deltab = static_cast<const float*>(uniform_ptr(delta + qh0 * Nq));
   const int nqt = (int)((Nq + C::kBQ - 1) / C::kBQ);
   const int ntiles = grp * nqt;
   const int tail = (int)(Nq - (nqt - 1) * C::kBQ);   // valid rows of a head's last tile

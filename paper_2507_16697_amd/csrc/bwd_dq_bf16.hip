@@ -96,8 +96,11 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
   if (bh >= BH) return;
 
   const int64_t kvh = kv_head(bh, H, grp);
-  const char* kb = reinterpret_cast<const char*>(k + kvh * Nk * D);
-  const char* vb = reinterpret_cast<const char*>(v + kvh * Nk * D);
+  // wave-uniform bases in SGPRs, so that the per-tile load addresses are scalar arithmetic
+  const char* kb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(k + kvh * Nk * D)));
+  const char* vb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(v + kvh * Nk * D)));
 
   // Tiles: chunk r covers keys [r Nk / R, (r+1) Nk / R), cut into 64-key tiles from its start.
   // ld_*: the next tile to load; nx_*: the tile after the one being computed.

@@ -104,16 +104,16 @@ __device__ __forceinline__ void issue_tile(const char* __restrict__ base, uint32
   if (start + C::kBK <= hi) {
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u)
-      load_lds16(src + goff[u],
-                 dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024));
+      load_lds16_s(src, (uint32_t)goff[u],
+                   dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024));
   } else {
     cold_path();
     const int last = (int)(hi - 1 - start);
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
       const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
-      load_lds16(src + off,
-                 dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024));
+      load_lds16_s(src, (uint32_t)off,
+                   dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024));
     }
   }
 }
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int wave = t >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int n = lane & 31;
   const int g = lane >> 5;
 
@@ -170,8 +170,11 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
 
   const __bf16* qb = q + bh * Nq * D;
   const int64_t kvh = kv_head(bh, H, grp);
-  const char* kb = reinterpret_cast<const char*>(k + kvh * Nk * D);
-  const char* vb = reinterpret_cast<const char*>(v + kvh * Nk * D);
+  // wave-uniform bases in SGPRs, so that the per-tile load addresses are scalar arithmetic
+  const char* kb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(k + kvh * Nk * D)));
+  const char* vb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(v + kvh * Nk * D)));
   int goff[C::kLoads], grow[C::kLoads];
   load_offsets<D>(goff, grow, wave, lane);
 
