@@ -183,6 +183,62 @@ ringx_status ringx_attn_bwd_dq(const void* q, const void* k, const void* v, cons
                                float scale, ringx_dtype dtype, hipStream_t stream);
 
 /*
+ * Backward through stored dS, bf16 with d = 128 (RINGX_E_UNSUPPORTED otherwise).  The same
+ * gradients as the recompute backward above (Sec. III-A: K/V chunk gradients per chunk, dQ
+ * accumulated over every chunk), computed in a different order: the dK/dV stage also writes every
+ * -dS_ij it forms (the bf16 operand of its dK product) to a caller-owned buffer, and the dQ stage
+ * forms dQ_i = scale sum_j dS_ij k_j from it instead of recomputing P and dP.  That is 7U of
+ * matrix products per backward instead of 9U (U = 2 B H Nq Nk d), for 2 B H Nq Nk bytes of dS
+ * written and read once.  Both stages work on a slab of consecutive K/V heads
+ * [kv_begin, kv_begin + kv_count) of the B * Hkv (batch-major; K/V head m serves query heads
+ * m G .. m G + G - 1, G = H / Hkv), so that the stored dS of one slab fits the buffer.  The layout
+ * of the buffer is private to the library: only ringx_attn_bwd_dq_ds reads it.
+ *
+ * ringx_bwd_ds_bytes: bytes of stored dS for kv_count K/V heads (about 2 G Nq Nk each); 0 if the
+ * arguments are invalid.  Host only.
+ */
+size_t ringx_bwd_ds_bytes(int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                          int64_t kv_count);
+
+/* dK/dV of the slab's K/V heads, as ringx_attn_bwd_dkdv (with Hkv K/V heads) restricted to them:
+ * rows of dk, dv [B,Hkv,Nk,d] fp32 outside the slab are not touched.  delta [2,B,H,Nq] from
+ * ringx_bwd_preprocess.  ds/ds_bytes: at least ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_count)
+ * bytes, 16-byte aligned; receives the slab's dS (previous contents ignored).
+ * RINGX_E_SHAPE if kv_begin < 0, kv_count < 1 or the slab passes B * Hkv; RINGX_E_WORKSPACE if
+ * ds is NULL or too small. */
+ringx_status ringx_attn_bwd_dkdv_ds(const void* q, const void* k, const void* v, const void* dout,
+                                    const float* lse, const float* delta, float* dk, float* dv,
+                                    void* ds, size_t ds_bytes, int64_t B, int64_t H, int64_t Hkv,
+                                    int64_t Nq, int64_t Nk, int64_t d, int64_t R, float scale,
+                                    ringx_dtype dtype, int accumulate_dkv, int64_t kv_begin,
+                                    int64_t kv_count, hipStream_t stream);
+
+/* dQ of the query heads of the slab's K/V heads from ds as written by ringx_attn_bwd_dkdv_ds with
+ * the same shapes and slab: dq [B,H,Nq,d] fp32, those rows overwritten, the others not touched.
+ * k [B,Hkv,Nk,d] bf16.  Errors as ringx_attn_bwd_dkdv_ds. */
+ringx_status ringx_attn_bwd_dq_ds(const void* ds, size_t ds_bytes, const void* k, float* dq,
+                                  int64_t B, int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk,
+                                  int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                  int64_t kv_begin, int64_t kv_count, hipStream_t stream);
+
+/* The whole backward through stored dS: ringx_bwd_preprocess, then ringx_attn_bwd_dkdv_ds and
+ * ringx_attn_bwd_dq_ds slab by slab, with as many K/V heads per slab as the workspace holds.
+ * Arguments as ringx_attn_bwd_gqa (Hkv = H for multi-head attention); the workspace must hold at
+ * least ringx_bwd_ds_workspace_bytes(B, H, Hkv, Nq, Nk, d, R, 1) bytes (the per-row statistics
+ * and one K/V head's dS); more lets a slab hold more heads.  dq, dk, dv agree with ringx_attn_bwd
+ * to rounding (dk, dv bitwise). */
+ringx_status ringx_attn_bwd_ds(const void* q, const void* k, const void* v, const void* out,
+                               const void* dout, const float* lse, float* dq, float* dk,
+                               float* dv, int64_t B, int64_t H, int64_t Hkv, int64_t Nq,
+                               int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                               int accumulate_dkv, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/* Workspace of ringx_attn_bwd_ds for slabs of kv_per_slab K/V heads (0 if invalid).  Host only. */
+size_t ringx_bwd_ds_workspace_bytes(int64_t B, int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk,
+                                    int64_t d, int64_t R, int64_t kv_per_slab);
+
+/*
  * One ring step of the forward (Sec. III-A: at every step a GPU holds one K/V chunk of S/N tokens,
  * computes its local result, and the results are merged by Eq. (5); "Communication and
  * computation overlap": the next chunk arrives in a second buffer meanwhile).  Computes the local

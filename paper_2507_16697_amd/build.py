@@ -19,7 +19,7 @@ LIB = os.path.join(PKG, "libringx.so")
 
 SOURCES = ["ringx_api.cpp", "fwd_bf16.hip", "fwd_f32.hip", "merge.hip", "bwd_pre.hip",
            "bwd_bf16.hip", "bwd_bf16_d64.hip", "bwd_dq_bf16.hip",
-           "bwd_dq_bf16_d64.hip", "bwd_f32.hip", "tt_tokenize.hip"]
+           "bwd_dq_bf16_d64.hip", "bwd_dq_ds.hip", "bwd_f32.hip", "tt_tokenize.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",

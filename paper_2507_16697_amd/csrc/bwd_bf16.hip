@@ -87,13 +87,13 @@ __device__ __forceinline__ int eoff(int row, int col) {
   return toff<RB>(row, col >> 3) + (col & 7) * 2;
 }
 
-template <int D>
+template <int D, bool kStore>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     const __bf16* __restrict__ q, const __bf16* __restrict__ k, const __bf16* __restrict__ v,
     const __bf16* __restrict__ dout, const float* __restrict__ nl,
     const float* __restrict__ delta, float* __restrict__ dk, float* __restrict__ dv, int BHkv,
     int H, int grp, int64_t Nq, int64_t Nk, int R, int tiles_per_chunk, float c2, float scale,
-    int accumulate) {
+    int accumulate, char* __restrict__ ds) {
   using C = DkvCfg<D>;
   __shared__ __attribute__((aligned(1024))) char lds[C::kLds];
   const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
@@ -412,13 +412,47 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
   dblk = read_d(0, 1);
   __builtin_amdgcn_sched_barrier(0);
 
+  // Store mode: the -dS operands of each tile's two 32-query blocks (B operands of the dK
+  // products: lane = key n, queries 16 ks + 4 g + (m & 3) + 8 (m >> 2) of the block in element m
+  // of sf[ks]) go to the stored-dS layout (ds_unit_offset), each 16-byte fragment at 16 * lane of
+  // its 1 KiB half-unit: block 0 of tile it once its dK products are issued, block 1 at the top
+  // of tile it+1 (its registers live until then), 4 KiB per wave and tile.  ds_w: this wave's key
+  // block in query group 0 of the first query head; ds_t: the current tile's units relative to
+  // it (query head st_j of the group, query tile st_qt of that head).
+  // (Offsets stay integers added to the kernel argument, so that the compiler keeps the stores
+  // global stores; a pointer rebuilt from integers would become a flat store, which also counts
+  // against the LDS wait counter.)
+  int64_t ds_w = 0, ds_t = 0, ds_head = 0, ds_grp = 0;
+  int st_j = 0, st_qt = 0;
+  if constexpr (kStore) {
+    const int64_t nqg = (Nq + 127) / 128;
+    const int64_t nkb = 4 * (int64_t)R * tiles_per_chunk;
+    const int64_t kb = ((int64_t)r * tiles_per_chunk + tile) * 4 + wave;
+    ds_w = ds_unit_offset(qh0, 0, kb, 0, nqg, nkb);
+    ds_grp = 4 * kDsUnitBytes;
+    ds_head = nkb * nqg * ds_grp;
+  }
+  auto ds_store = [&](int64_t off, const bf16x8& x) {
+    *reinterpret_cast<u32x4*>(ds + (ds_w + off) + 16 * lane) = __builtin_bit_cast(u32x4, x);
+  };
+
   for (int it = 0; it < ntiles; ++it) {
     const int st_cur = (int)(it & 3) * C::kStage;
     const int st_nxt = (int)((it + 1) & 3) * C::kStage;
-    // tile it+1 landed (tile it+2 may stay in flight); every wave is done with tile it-1
+    // tile it+1 landed (tile it+2 may stay in flight); every wave is done with tile it-1.  In
+    // store mode the stores issued after tile it+1's loads also count: block 0 of tile it-2
+    // (it >= 2), block 1 of tile it-2 (it >= 2) and block 0 of tile it-1 (it >= 1), two each.
     if (it + 2 < ntiles) {
-      if (wave < 2) wait_vmem<C::kTileOps + 1>();
-      else wait_vmem<C::kTileOps>();
+      if (!kStore || it == 0) {
+        if (wave < 2) wait_vmem<C::kTileOps + 1>();
+        else wait_vmem<C::kTileOps>();
+      } else if (it == 1) {
+        if (wave < 2) wait_vmem<C::kTileOps + 3>();
+        else wait_vmem<C::kTileOps + 2>();
+      } else {
+        if (wave < 2) wait_vmem<C::kTileOps + 7>();
+        else wait_vmem<C::kTileOps + 6>();
+      }
     } else {
       wait_vmem<0>();
     }
@@ -430,6 +464,18 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
       zero_tail((int)((it + 1) & 3));
       __syncthreads();
     }
+    if constexpr (kStore) {
+      if (it > 0) {
+        ds_store(ds_t + kDsUnitBytes, sfb[0]);
+        ds_store(ds_t + kDsUnitBytes + 1024, sfb[1]);
+      }
+      // units of tile it: query group st_qt / 2 of head st_j, blocks 2 (st_qt % 2) + 0, 1
+      ds_t = st_j * ds_head + (st_qt >> 1) * ds_grp + (st_qt & 1) * 2 * kDsUnitBytes;
+      if (++st_qt == nqt) {
+        st_qt = 0;
+        ++st_j;
+      }
+    }
     if (it + 3 < ntiles) issue_next((int)((it + 3) & 3));
     __builtin_amdgcn_sched_barrier(0);
 
@@ -437,10 +483,18 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     // the last tile, whose results are not used)
     phase1(sa, pa, sb, pb, pfa[1], sfa[1], st_cur, 0, st_cur, 1);
     phase2(pfa, sfa, sb, pb, pfb[0], sfb[0], st_cur, 0, st_cur, 1, st_nxt, 0);
+    if constexpr (kStore) {
+      ds_store(ds_t, sfa[0]);
+      ds_store(ds_t + 1024, sfa[1]);
+    }
     phase1(sb, pb, sa, pa, pfb[1], sfb[1], st_cur, 1, st_nxt, 0);
     phase2(pfb, sfb, sa, pa, pfa[0], sfa[0], st_cur, 1, st_nxt, 0, st_nxt, 1);
     // after the last products, before any code at the loop exit reads or moves the accumulators
     if (it + 1 == ntiles) asm volatile("s_nop 15\n\ts_nop 15");
+  }
+  if constexpr (kStore) {
+    ds_store(ds_t + kDsUnitBytes, sfb[0]);
+    ds_store(ds_t + kDsUnitBytes + 1024, sfb[1]);
   }
 
   if (key_ok) {
@@ -465,24 +519,25 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
   }
 }
 
-template <int D>
+template <int D, bool kStore>
 hipError_t launch(const BwdArgs& a) {
   using C = DkvCfg<D>;
   const int64_t max_chunk = (a.Nk + a.R - 1) / a.R;
   const int64_t tpc = (max_chunk + C::kBK - 1) / C::kBK;
+  static_assert(C::kBK == 128, "stored-dS layout: 128-key tiles");
   const int64_t nwg = a.BH / a.G * a.R * tpc;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((uint32_t)nwg), dim3(C::kThreads), 0, a.stream,
-                     (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, kStore>), dim3((uint32_t)nwg), dim3(C::kThreads), 0,
+                     a.stream, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
                      (const __bf16*)a.dout, a.nl, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
                      (int)a.H, (int)a.G, a.Nq, a.Nk, (int)a.R, (int)tpc, a.scale * kLog2e,
-                     a.scale, a.accumulate_dkv ? 1 : 0);
+                     a.scale, a.accumulate_dkv ? 1 : 0, a.ds);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_bwd_dkdv_bf16(const BwdArgs& a) {
-  if (a.d == 128) return launch<128>(a);
+  if (a.d == 128) return a.ds ? launch<128, true>(a) : launch<128, false>(a);
   return launch_bwd_dkdv_bf16_d64(a);
 }
 

@@ -359,6 +359,182 @@ ringx_status ringx_attn_bwd_gqa(const void* q, const void* k, const void* v, con
                   accumulate_dkv, workspace, workspace_bytes, stream);
 }
 
+size_t ringx_bwd_ds_bytes(int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
+                          int64_t kv_count) {
+  if (Hkv < 1 || H < 1 || H % Hkv != 0 || kv_count < 1) return 0;
+  if (check_dims(1, H, Nq, Nk, d, R, 1.0f, RINGX_BF16) != RINGX_OK || d != 128) return 0;
+  int64_t nh, x;
+  if (!mul_ok(kv_count, H / Hkv, &nh)) return 0;
+  // nh query heads x ceil(Nq/128) groups x 4 R tpc key blocks x 4 units of 2 KiB
+  const int64_t tpc = ringx::ds_tiles_per_chunk(Nk, R);
+  if (!mul_ok(nh, (Nq + 127) / 128, &x) || !mul_ok(x, 16 * R, &x) || !mul_ok(x, tpc, &x))
+    return 0;
+  if (x > (int64_t(1) << 62) / ringx::kDsUnitBytes) return 0;
+  return static_cast<size_t>(ringx::ds_bytes(nh, Nq, Nk, R));
+}
+
+size_t ringx_bwd_ds_workspace_bytes(int64_t B, int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk,
+                                    int64_t d, int64_t R, int64_t kv_per_slab) {
+  if (B < 1 || Hkv < 1 || kv_per_slab < 1 || kv_per_slab > B * Hkv) return 0;
+  const size_t stats = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, RINGX_BF16);
+  const size_t ds = ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_per_slab);
+  if (stats == 0 || ds == 0) return 0;
+  return stats + ds;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Validation shared by the two stored-dS stages: shapes, the slab [kv_begin, kv_begin +
+// kv_count) of the B * Hkv K/V heads, and the stored-dS buffer.
+ringx_status check_ds_common(const void* ds, size_t ds_bytes, int64_t B, int64_t H, int64_t Hkv,
+                             int64_t Nq, int64_t Nk, int64_t d, int64_t R, float scale,
+                             ringx_dtype dtype, int64_t kv_begin, int64_t kv_count) {
+  if (Hkv < 1 || H < 1 || H % Hkv != 0) return RINGX_E_SHAPE;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  if (dtype != RINGX_BF16 || d != 128) return RINGX_E_UNSUPPORTED;
+  if (kv_begin < 0 || kv_count < 1 || kv_begin > B * Hkv - kv_count) return RINGX_E_SHAPE;
+  const size_t need = ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_count);
+  if (need == 0) return RINGX_E_SHAPE;
+  if (!ds || ds_bytes < need) return RINGX_E_WORKSPACE;
+  if (!aligned16(ds)) return RINGX_E_ALIGN;
+  // the dQ grid: one workgroup per (query head, 128 queries)
+  if (kv_count * (H / Hkv) * ((Nq + 127) / 128) > 0xffffffffll) return RINGX_E_SHAPE;
+  return RINGX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ringx_status ringx_attn_bwd_dkdv_ds(const void* q, const void* k, const void* v, const void* dout,
+                                    const float* lse, const float* delta, float* dk, float* dv,
+                                    void* ds, size_t ds_bytes, int64_t B, int64_t H, int64_t Hkv,
+                                    int64_t Nq, int64_t Nk, int64_t d, int64_t R, float scale,
+                                    ringx_dtype dtype, int accumulate_dkv, int64_t kv_begin,
+                                    int64_t kv_count, hipStream_t stream) {
+  if (!q || !k || !v || !dout || !lse || !delta || !dk || !dv) return RINGX_E_NULLPTR;
+  ringx_status st = check_ds_common(ds, ds_bytes, B, H, Hkv, Nq, Nk, d, R, scale, dtype,
+                                    kv_begin, kv_count);
+  if (st != RINGX_OK) return st;
+  for (const void* p : {q, k, v, dout, (const void*)lse, (const void*)delta, (const void*)dk,
+                        (const void*)dv})
+    if (!aligned16(p)) return RINGX_E_ALIGN;
+  const int64_t bh = B * H, bkv = B * Hkv, G = H / Hkv;
+  const size_t need = ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_count);
+  const Span ins[] = {span(q, bh * Nq * d * 2),    span(k, bkv * Nk * d * 2),
+                      span(v, bkv * Nk * d * 2),   span(dout, bh * Nq * d * 2),
+                      span(lse, bh * Nq * 4),      span(delta, 2 * bh * Nq * 4)};
+  const Span outs[] = {span(dk, bkv * Nk * d * 4), span(dv, bkv * Nk * d * 4),
+                       span(ds, (int64_t)need)};
+  for (int i = 0; i < 3; ++i) {
+    for (const Span& s : ins)
+      if (overlap(outs[i], s)) return RINGX_E_ALIAS;
+    for (int j = i + 1; j < 3; ++j)
+      if (overlap(outs[i], outs[j])) return RINGX_E_ALIAS;
+  }
+  // the slab as a batch of kv_count K/V heads with G query heads each (query head h of K/V head
+  // m is m G + h in batch-major order)
+  const int64_t q0 = kv_begin * G;
+  ringx::BwdArgs a;
+  a.q = static_cast<const char*>(q) + q0 * Nq * d * 2;
+  a.dout = static_cast<const char*>(dout) + q0 * Nq * d * 2;
+  a.k = static_cast<const char*>(k) + kv_begin * Nk * d * 2;
+  a.v = static_cast<const char*>(v) + kv_begin * Nk * d * 2;
+  a.dk = dk + kv_begin * Nk * d, a.dv = dv + kv_begin * Nk * d;
+  a.delta = const_cast<float*>(delta) + q0 * Nq;
+  a.nl = const_cast<float*>(delta) + bh * Nq + q0 * Nq;
+  a.ds = static_cast<char*>(ds);
+  a.BH = kv_count * G, a.Nq = Nq, a.Nk = Nk, a.d = d, a.R = R, a.scale = scale;
+  a.H = G, a.G = G;
+  a.accumulate_dkv = accumulate_dkv != 0, a.stream = stream;
+  return hip_status(ringx::launch_bwd_dkdv_bf16(a));
+}
+
+ringx_status ringx_attn_bwd_dq_ds(const void* ds, size_t ds_bytes, const void* k, float* dq,
+                                  int64_t B, int64_t H, int64_t Hkv, int64_t Nq, int64_t Nk,
+                                  int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                                  int64_t kv_begin, int64_t kv_count, hipStream_t stream) {
+  if (!k || !dq) return RINGX_E_NULLPTR;
+  ringx_status st = check_ds_common(ds, ds_bytes, B, H, Hkv, Nq, Nk, d, R, scale, dtype,
+                                    kv_begin, kv_count);
+  if (st != RINGX_OK) return st;
+  if (!aligned16(k) || !aligned16(dq)) return RINGX_E_ALIGN;
+  const int64_t bh = B * H, bkv = B * Hkv, G = H / Hkv;
+  const size_t need = ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_count);
+  const Span so = span(dq, bh * Nq * d * 4);
+  if (overlap(so, span(ds, (int64_t)need)) || overlap(so, span(k, bkv * Nk * d * 2)))
+    return RINGX_E_ALIAS;
+  ringx::DsArgs a;
+  a.ds = ds;
+  a.k = static_cast<const char*>(k) + kv_begin * Nk * d * 2;
+  a.dq = dq + kv_begin * G * Nq * d;
+  a.nh = kv_count * G, a.G = G, a.Nq = Nq, a.Nk = Nk, a.R = R;
+  a.tpc = ringx::ds_tiles_per_chunk(Nk, R), a.scale = scale, a.stream = stream;
+  return hip_status(ringx::launch_bwd_dq_ds(a));
+}
+
+ringx_status ringx_attn_bwd_ds(const void* q, const void* k, const void* v, const void* out,
+                               const void* dout, const float* lse, float* dq, float* dk,
+                               float* dv, int64_t B, int64_t H, int64_t Hkv, int64_t Nq,
+                               int64_t Nk, int64_t d, int64_t R, float scale, ringx_dtype dtype,
+                               int accumulate_dkv, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream) {
+  if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv) return RINGX_E_NULLPTR;
+  if (Hkv < 1 || H < 1 || H % Hkv != 0) return RINGX_E_SHAPE;
+  ringx_status st = check_dims(B, H, Nq, Nk, d, R, scale, dtype);
+  if (st != RINGX_OK) return st;
+  if (dtype != RINGX_BF16 || d != 128) return RINGX_E_UNSUPPORTED;
+  const size_t stats = ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, dtype);
+  const size_t per_kv = ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, 1);
+  if (stats == 0 || per_kv == 0) return RINGX_E_SHAPE;
+  if (!workspace || workspace_bytes < stats + per_kv) return RINGX_E_WORKSPACE;
+  for (const void* p : {q, k, v, out, dout, (const void*)lse, (const void*)dq, (const void*)dk,
+                        (const void*)dv, (const void*)workspace})
+    if (!aligned16(p)) return RINGX_E_ALIGN;
+  const int64_t bh = B * H, bkv = B * Hkv;
+  // as many K/V heads per slab as the workspace holds (and the dQ grid allows)
+  const int64_t wg_per_kv = (H / Hkv) * ((Nq + 127) / 128);
+  if (wg_per_kv > 0xffffffffll) return RINGX_E_SHAPE;
+  int64_t per_slab = (int64_t)((workspace_bytes - stats) / per_kv);
+  if (per_slab > bkv) per_slab = bkv;
+  if (per_slab > 0xffffffffll / wg_per_kv) per_slab = 0xffffffffll / wg_per_kv;
+  while (per_slab > 1 && ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, per_slab) == 0) --per_slab;
+  const size_t used = stats + ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, per_slab);
+  const Span ins[] = {span(q, bh * Nq * d * 2),    span(k, bkv * Nk * d * 2),
+                      span(v, bkv * Nk * d * 2),   span(out, bh * Nq * d * 2),
+                      span(dout, bh * Nq * d * 2), span(lse, bh * Nq * 4)};
+  const Span outs[] = {span(dq, bh * Nq * d * 4), span(dk, bkv * Nk * d * 4),
+                       span(dv, bkv * Nk * d * 4), span(workspace, (int64_t)used)};
+  for (int i = 0; i < 4; ++i) {
+    for (const Span& s : ins)
+      if (overlap(outs[i], s)) return RINGX_E_ALIAS;
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(outs[i], outs[j])) return RINGX_E_ALIAS;
+  }
+  float* delta = static_cast<float*>(workspace);
+  char* ds = static_cast<char*>(workspace) + stats;
+  const size_t ds_cap = workspace_bytes - stats;
+  {
+    ringx::BwdArgs a;
+    a.out = out, a.dout = dout, a.lse = lse, a.delta = delta, a.nl = delta + bh * Nq;
+    a.BH = bh, a.Nq = Nq, a.Nk = 1, a.d = d, a.R = 1, a.stream = stream, a.H = H, a.G = 1;
+    if (ringx::launch_bwd_pre(a, true) != hipSuccess) return RINGX_E_HIP;
+  }
+  for (int64_t kv0 = 0; kv0 < bkv; kv0 += per_slab) {
+    const int64_t cnt = kv0 + per_slab <= bkv ? per_slab : bkv - kv0;
+    st = ringx_attn_bwd_dkdv_ds(q, k, v, dout, lse, delta, dk, dv, ds, ds_cap, B, H, Hkv, Nq, Nk,
+                                d, R, scale, dtype, accumulate_dkv, kv0, cnt, stream);
+    if (st != RINGX_OK) return st == RINGX_E_HIP ? st : RINGX_E_HIP;
+    st = ringx_attn_bwd_dq_ds(ds, ds_cap, k, dq, B, H, Hkv, Nq, Nk, d, R, scale, dtype, kv0, cnt,
+                              stream);
+    if (st != RINGX_OK) return st == RINGX_E_HIP ? st : RINGX_E_HIP;
+  }
+  return RINGX_OK;
+}
+
 ringx_status ringx_attn_fwd_step(const void* q, const void* k, const void* v, float* out_acc,
                                  float* lse_acc, int64_t B, int64_t H, int64_t Nq, int64_t Nk,
                                  int64_t d, float scale, ringx_dtype dtype, int first,

@@ -58,6 +58,35 @@ struct BwdArgs {
   float scale = 1.f;
   bool accumulate_dkv = false;  // dk, dv += instead of =
   bool accumulate_dq = false;   // dq += instead of =
+  char* ds = nullptr;           // store mode of the dK/dV kernel: -dS of every score, bf16
+  hipStream_t stream = nullptr;
+};
+
+// Stored dS (written by the dK/dV kernel in store mode, read by bwd_dq_ds.hip): per query head j,
+// 32-key block kb of the padded key axis (chunk r, 128-key tile t, block w: kb = 4 (r tpc + t) + w,
+// nkb = 4 R tpc blocks), 128-query group qg and 32-query block qs of the group, one unit of
+// kDsUnitBytes.  The query axis runs fastest, so that each wave of the writer, which owns one key
+// block and sweeps the queries, writes one contiguous stream.
+constexpr int64_t kDsUnitBytes = 2048;
+__host__ __device__ inline int64_t ds_unit_offset(int64_t j, int64_t qg, int64_t kb, int64_t qs,
+                                                  int64_t nqg, int64_t nkb) {
+  return (((j * nkb + kb) * nqg + qg) * 4 + qs) * kDsUnitBytes;
+}
+// 128-key tiles per chunk (the longest chunk, ceil(Nk / R) keys, rounded up)
+__host__ __device__ inline int64_t ds_tiles_per_chunk(int64_t Nk, int64_t R) {
+  return ((Nk + R - 1) / R + 127) / 128;
+}
+// bytes of stored dS for nh query heads
+inline int64_t ds_bytes(int64_t nh, int64_t Nq, int64_t Nk, int64_t R) {
+  return nh * ((Nq + 127) / 128) * 4 * R * ds_tiles_per_chunk(Nk, R) * 4 * kDsUnitBytes;
+}
+
+struct DsArgs {
+  const void* ds = nullptr;     // stored -dS of nh query heads
+  const void* k = nullptr;      // K of the nh / G K/V heads, [nh / G, Nk, 128] bf16
+  float* dq = nullptr;          // [nh, Nq, 128] fp32, overwritten
+  int64_t nh = 0, G = 1, Nq = 0, Nk = 0, R = 1, tpc = 1;
+  float scale = 1.f;
   hipStream_t stream = nullptr;
 };
 
@@ -87,6 +116,7 @@ hipError_t launch_bwd_dq_bf16(const BwdArgs& a);
 hipError_t launch_bwd_dq_bf16_d64(const BwdArgs& a);   // d = 64 (bwd_dq_bf16_d64.hip)
 hipError_t launch_bwd_dkdv_f32(const BwdArgs& a);
 hipError_t launch_bwd_dq_f32(const BwdArgs& a);
+hipError_t launch_bwd_dq_ds(const DsArgs& a);   // d = 128, bf16 dS (bwd_dq_ds.hip)
 
 hipError_t launch_tt_tokenize(const TokArgs& a);
 

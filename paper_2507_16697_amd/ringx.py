@@ -40,7 +40,9 @@ EXPORTED = ("ringx_attn_fwd", "ringx_attn_fwd_partials", "ringx_lse_merge", "rin
             "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv", "ringx_attn_bwd_dq",
             "ringx_attn_fwd_step", "ringx_attn_bwd_step", "ringx_attn_fwd_gqa",
             "ringx_attn_bwd_gqa", "ringx_tt_tokenize", "ringx_bwd_workspace_bytes",
-            "ringx_chunk_bounds", "ringx_status_str", "ringx_attn_bwd_noalloc")
+            "ringx_chunk_bounds", "ringx_status_str", "ringx_attn_bwd_noalloc",
+            "ringx_bwd_ds_bytes", "ringx_attn_bwd_dkdv_ds", "ringx_attn_bwd_dq_ds",
+            "ringx_attn_bwd_ds", "ringx_bwd_ds_workspace_bytes")
 
 
 class RingxError(RuntimeError):
@@ -92,6 +94,16 @@ def lib() -> ctypes.CDLL:
                                         ctypes.c_float, ctypes.c_int, _P]
         L.ringx_bwd_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, ctypes.c_int]
         L.ringx_bwd_workspace_bytes.restype = ctypes.c_size_t
+        L.ringx_bwd_ds_bytes.argtypes = [_I, _I, _I, _I, _I, _I, _I]
+        L.ringx_bwd_ds_bytes.restype = ctypes.c_size_t
+        L.ringx_bwd_ds_workspace_bytes.argtypes = [_I, _I, _I, _I, _I, _I, _I, _I]
+        L.ringx_bwd_ds_workspace_bytes.restype = ctypes.c_size_t
+        L.ringx_attn_bwd_dkdv_ds.argtypes = [_P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                             _I, _I, _I, _I, _I, _I, _I, ctypes.c_float,
+                                             ctypes.c_int, ctypes.c_int, _I, _I, _P]
+        L.ringx_attn_bwd_dq_ds.argtypes = [_P, ctypes.c_size_t, _P, _P, _I, _I, _I, _I, _I, _I,
+                                           _I, ctypes.c_float, ctypes.c_int, _I, _I, _P]
+        L.ringx_attn_bwd_ds.argtypes = L.ringx_attn_bwd_gqa.argtypes
         L.ringx_chunk_bounds.argtypes = [_I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_I)]
         L.ringx_status_str.argtypes = [ctypes.c_int]
         L.ringx_status_str.restype = ctypes.c_char_p
@@ -99,7 +111,8 @@ def lib() -> ctypes.CDLL:
                      "ringx_attn_bwd", "ringx_bwd_preprocess", "ringx_attn_bwd_dkdv",
                      "ringx_attn_bwd_dq", "ringx_attn_fwd_step", "ringx_attn_bwd_step",
                      "ringx_attn_fwd_gqa", "ringx_attn_bwd_gqa", "ringx_tt_tokenize",
-                     "ringx_chunk_bounds", "ringx_attn_bwd_noalloc"):
+                     "ringx_chunk_bounds", "ringx_attn_bwd_noalloc", "ringx_attn_bwd_dkdv_ds",
+                     "ringx_attn_bwd_dq_ds", "ringx_attn_bwd_ds"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -122,6 +135,14 @@ def ringx_chunk_bounds(Nk: int, R: int, r: int) -> tuple[int, int]:
 
 def ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, dtype) -> int:
     return int(lib().ringx_bwd_workspace_bytes(B, H, Nq, Nk, d, R, int(dtype)))
+
+
+def ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_count) -> int:
+    return int(lib().ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, d, R, kv_count))
+
+
+def ringx_bwd_ds_workspace_bytes(B, H, Hkv, Nq, Nk, d, R, kv_per_slab) -> int:
+    return int(lib().ringx_bwd_ds_workspace_bytes(B, H, Hkv, Nq, Nk, d, R, kv_per_slab))
 
 
 # ---------------------------------------------------------------------------------------------
@@ -459,6 +480,96 @@ def ringx_attn_bwd_gqa(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=
                                   _dtype_code(q), 1 if accumulate_dkv else 0, ws.data_ptr(),
                                   ws.numel(), _stream(stream))
     _check("ringx_attn_bwd_gqa", st)
+    return dq, dk, dv
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def ringx_attn_bwd_dkdv_ds(q, k, v, dout, lse, delta, R: int, ds, kv_begin: int, kv_count: int,
+                           scale=None, dk=None, dv=None, accumulate_dkv=False, stream=None):
+    """dK/dV of K/V heads [kv_begin, kv_begin + kv_count) (of B * Hkv), writing their query
+    heads' dS into the uint8 device buffer ds (ringx_bwd_ds_bytes(...) bytes).  Returns fp32
+    (dk, dv) [B,Hkv,Nk,d]; rows of other heads are not touched."""
+    torch = _torch()
+    _dev(q, k, v, dout, lse, delta, ds)
+    B, H, Hkv, Nq, Nk, d = _qkv(q, k, v, heads_kv=True)
+    _check_grad_inputs(q, dout, lse, delta)
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dk = torch.zeros((B, Hkv, Nk, d), **f32) if dk is None else dk
+    dv = torch.zeros((B, Hkv, Nk, d), **f32) if dv is None else dv
+    _dev(dk, dv)
+    _expect("dk", dk, (B, Hkv, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, Hkv, Nk, d), torch.float32, q.device)
+    if ds.device != q.device:
+        raise ValueError(f"ds: on {ds.device}, expected {q.device}")
+    st = lib().ringx_attn_bwd_dkdv_ds(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(),
+                                      lse.data_ptr(), delta.data_ptr(), dk.data_ptr(),
+                                      dv.data_ptr(), ds.data_ptr(), _nbytes(ds), B, H, Hkv, Nq,
+                                      Nk, d, R, _scale(scale, d), _dtype_code(q),
+                                      1 if accumulate_dkv else 0, kv_begin, kv_count,
+                                      _stream(stream))
+    _check("ringx_attn_bwd_dkdv_ds", st)
+    return dk, dv
+
+
+def ringx_attn_bwd_dq_ds(ds, k, q_shape, R: int, kv_begin: int, kv_count: int, scale=None,
+                         dq=None, stream=None):
+    """dQ of the query heads of K/V heads [kv_begin, kv_begin + kv_count) from ds as written by
+    ringx_attn_bwd_dkdv_ds.  q_shape = (B, H, Nq, d).  Returns fp32 dq [B,H,Nq,d] (rows of other
+    heads are not touched)."""
+    torch = _torch()
+    _dev(ds, k)
+    B, H, Nq, d = (int(x) for x in q_shape)
+    if k.dim() != 4 or k.shape[0] != B or k.shape[3] != d:
+        raise ValueError(f"k: shape {tuple(k.shape)} does not match q_shape {tuple(q_shape)}")
+    Hkv, Nk = int(k.shape[1]), int(k.shape[2])
+    if dq is None:
+        dq = torch.empty((B, H, Nq, d), dtype=torch.float32, device=k.device)
+    _dev(dq)
+    _expect("dq", dq, (B, H, Nq, d), torch.float32, k.device)
+    if ds.device != k.device:
+        raise ValueError(f"ds: on {ds.device}, expected {k.device}")
+    st = lib().ringx_attn_bwd_dq_ds(ds.data_ptr(), _nbytes(ds), k.data_ptr(), dq.data_ptr(), B, H,
+                                    Hkv, Nq, Nk, d, R, _scale(scale, d), _dtype_code(k),
+                                    kv_begin, kv_count, _stream(stream))
+    _check("ringx_attn_bwd_dq_ds", st)
+    return dq
+
+
+def ringx_attn_bwd_ds(q, k, v, out, dout, lse, R: int, scale=None, dq=None, dk=None, dv=None,
+                      accumulate_dkv=False, workspace=None, kv_per_slab=2, stream=None):
+    """The backward through stored dS (bf16, d = 128): fp32 (dq, dk, dv), dk/dv [B,Hkv,Nk,d].
+    Without a workspace, one of ringx_bwd_ds_workspace_bytes(..., kv_per_slab) bytes is
+    allocated (slabs of kv_per_slab K/V heads, fewer if B * Hkv is smaller)."""
+    torch = _torch()
+    _dev(q, k, v, out, dout, lse)
+    B, H, Hkv, Nq, Nk, d = _qkv(q, k, v, heads_kv=True)
+    _expect("out", out, q.shape, q.dtype, q.device)
+    _expect("dout", dout, q.shape, q.dtype, q.device)
+    _expect("lse", lse, (B, H, Nq), torch.float32, q.device)
+    f32 = dict(dtype=torch.float32, device=q.device)
+    dq = torch.empty((B, H, Nq, d), **f32) if dq is None else dq
+    dk = torch.zeros((B, Hkv, Nk, d), **f32) if dk is None else dk
+    dv = torch.zeros((B, Hkv, Nk, d), **f32) if dv is None else dv
+    _dev(dq, dk, dv)
+    _expect("dq", dq, (B, H, Nq, d), torch.float32, q.device)
+    _expect("dk", dk, (B, Hkv, Nk, d), torch.float32, q.device)
+    _expect("dv", dv, (B, Hkv, Nk, d), torch.float32, q.device)
+    if workspace is None:
+        nbytes = ringx_bwd_ds_workspace_bytes(B, H, Hkv, Nq, Nk, d, R,
+                                              max(1, min(int(kv_per_slab), B * Hkv)))
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=q.device)
+    _dev(workspace)
+    if workspace.device != q.device:
+        raise ValueError(f"workspace: on {workspace.device}, expected {q.device}")
+    st = lib().ringx_attn_bwd_ds(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                 dout.data_ptr(), lse.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                 dv.data_ptr(), B, H, Hkv, Nq, Nk, d, R, _scale(scale, d),
+                                 _dtype_code(q), 1 if accumulate_dkv else 0, workspace.data_ptr(),
+                                 _nbytes(workspace), _stream(stream))
+    _check("ringx_attn_bwd_ds", st)
     return dq, dk, dv
 
 

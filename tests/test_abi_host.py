@@ -185,6 +185,74 @@ def test_gradient_stage_validation():
     assert dqs(dq=LP + 8 * GB + 800) == ALIAS    # dq over delta's second row (nl)
 
 
+def test_stored_ds_sizes():
+    """Stored dS: 2 KiB per (query head, 32-query block, 32-key block) of the padded axes: the
+    queries padded to 128 per head and every chunk's keys to whole 128-key tiles."""
+    def pad(x, m):
+        return -(-x // m) * m
+    for H, Hkv, Nq, Nk, R, kv in [(1, 1, 128, 128, 1, 1), (2, 2, 200, 777, 3, 2), (4, 2, 130, 300, 5, 1),
+                                   (16, 16, 32768, 262144, 8, 2), (4, 1, 64, 129, 1, 1)]:
+        G = H // Hkv
+        per_chunk = pad(-(-Nk // R), 128)
+        want = kv * G * pad(Nq, 128) * R * per_chunk * 2
+        assert ringx.ringx_bwd_ds_bytes(H, Hkv, Nq, Nk, 128, R, kv) == want
+    assert ringx.ringx_bwd_ds_bytes(16, 16, 32768, 262144, 128, 8, 1) == 16 << 30
+    # invalid: head dim 64, Hkv not dividing H, no heads, R > Nk
+    assert ringx.ringx_bwd_ds_bytes(2, 2, 100, 300, 64, 3, 1) == 0
+    assert ringx.ringx_bwd_ds_bytes(4, 3, 100, 300, 128, 3, 1) == 0
+    assert ringx.ringx_bwd_ds_bytes(2, 2, 100, 300, 128, 3, 0) == 0
+    assert ringx.ringx_bwd_ds_bytes(2, 2, 100, 300, 128, 301, 1) == 0
+    stats = ringx.ringx_bwd_workspace_bytes(2, 4, 100, 300, 128, 3, BF16)
+    assert ringx.ringx_bwd_ds_workspace_bytes(2, 4, 2, 100, 300, 128, 3, 3) == \
+        stats + ringx.ringx_bwd_ds_bytes(4, 2, 100, 300, 128, 3, 3)
+    assert ringx.ringx_bwd_ds_workspace_bytes(2, 4, 2, 100, 300, 128, 3, 5) == 0   # > B * Hkv
+
+
+DSP = OP + 32 * GB       # a fake stored-dS buffer
+
+
+def dkdv_ds(ds=DSP, dsb=1 << 30, dk=OP, dv=OP + 8 * GB, delta=LP + 8 * GB, kv0=0, kvn=2, H=4,
+            Hkv=2, B=1, d=128, dt=BF16, R=3, q=QP):
+    return ringx.lib().ringx_attn_bwd_dkdv_ds(q, KP, VP, QP + 16 * GB, LP, delta, dk, dv, ds, dsb,
+                                              B, H, Hkv, 100, 300, d, R, 0.125, dt, 0, kv0, kvn,
+                                              None)
+
+
+def dq_ds(ds=DSP, dsb=1 << 30, dq=OP, kv0=0, kvn=2, H=4, Hkv=2, B=1, d=128, dt=BF16, k=KP):
+    return ringx.lib().ringx_attn_bwd_dq_ds(ds, dsb, k, dq, B, H, Hkv, 100, 300, d, 3, 0.125, dt,
+                                            kv0, kvn, None)
+
+
+def bwd_ds(ws=VP + 32 * GB, wsb=1 << 30, dq=OP, dk=OP + 8 * GB, dv=OP + 16 * GB, d=128, dt=BF16,
+           Hkv=2):
+    return ringx.lib().ringx_attn_bwd_ds(QP, KP, VP, QP + 8 * GB, QP + 16 * GB, LP, dq, dk, dv, 1,
+                                         4, Hkv, 100, 300, d, 3, 0.125, dt, 0, ws, wsb, None)
+
+
+def test_stored_ds_validation():
+    need = ringx.ringx_bwd_ds_bytes(4, 2, 100, 300, 128, 3, 2)
+    assert dkdv_ds(q=0) == NULLPTR and dkdv_ds(dk=0) == NULLPTR and dq_ds(dq=0) == NULLPTR
+    assert dq_ds(k=0) == NULLPTR and bwd_ds(dq=0) == NULLPTR
+    assert dkdv_ds(ds=0) == WORKSPACE and dq_ds(ds=0) == WORKSPACE
+    assert dkdv_ds(dsb=need - 1) == WORKSPACE and dq_ds(dsb=need - 1) == WORKSPACE
+    # the slab must lie inside the B * Hkv K/V heads
+    assert dkdv_ds(kv0=-1) == SHAPE and dkdv_ds(kvn=0) == SHAPE and dkdv_ds(kv0=1, kvn=2) == SHAPE
+    assert dq_ds(kv0=2, kvn=1) == SHAPE and dkdv_ds(B=2, kv0=3, kvn=2) == SHAPE
+    assert dkdv_ds(Hkv=3) == SHAPE and dq_ds(Hkv=3) == SHAPE and bwd_ds(Hkv=3) == SHAPE
+    # bf16 with d = 128 only
+    for fn in (dkdv_ds, dq_ds, bwd_ds):
+        assert fn(d=64) == UNSUP and fn(dt=FP32) == UNSUP
+    assert dkdv_ds(R=301) == CHUNKS
+    assert dkdv_ds(ds=DSP + 8) == ALIGN and dq_ds(dq=OP + 4) == ALIGN
+    assert dkdv_ds(ds=QP) == ALIAS and dkdv_ds(ds=OP + 8 * GB - 64) == ALIAS   # ds over q, dv
+    assert dq_ds(dq=DSP) == ALIAS and dq_ds(dq=KP) == ALIAS
+    # the whole backward: the per-row statistics and one K/V head's dS at least
+    one = ringx.ringx_bwd_ds_workspace_bytes(1, 4, 2, 100, 300, 128, 3, 1)
+    assert bwd_ds(ws=0) == WORKSPACE and bwd_ds(wsb=one - 1) == WORKSPACE
+    assert bwd_ds(ws=VP + 32 * GB + 8) == ALIGN
+    assert bwd_ds(ws=OP + 16 * GB) == ALIAS and bwd_ds(dk=OP) == ALIAS
+
+
 def fstep(q=QP, k=KP, v=VP, o=OP, l=LP, B=1, H=2, Nq=100, Nk=300, d=64, scale=0.125, dt=BF16,
           first=1):
     return ringx.lib().ringx_attn_fwd_step(q, k, v, o, l, B, H, Nq, Nk, d, scale, dt, first, None)

@@ -25,7 +25,7 @@ def _asm(src, tmp_path):
 
 
 @pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip", "bwd_dq_bf16.hip",
-                                 "bwd_dq_bf16_d64.hip"])
+                                 "bwd_dq_bf16_d64.hip", "bwd_dq_ds.hip"])
 def test_m0_only_feeds_direct_lds_loads(src, tmp_path):
     lines = [l.strip() for l in _asm(src, tmp_path).splitlines()]
     code = [l for l in lines if l and not l.startswith(";") and not l.startswith(".")]
@@ -39,11 +39,23 @@ def test_m0_only_feeds_direct_lds_loads(src, tmp_path):
 
 
 @pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip", "bwd_dq_bf16.hip",
-                                 "bwd_dq_bf16_d64.hip", "merge.hip", "bwd_pre.hip"])
+                                 "bwd_dq_bf16_d64.hip", "bwd_dq_ds.hip", "merge.hip", "bwd_pre.hip"])
 def test_no_packed_fp32_and_no_scalar_stores(src, tmp_path):
     text = _asm(src, tmp_path)
     assert not re.search(r"\bv_pk_(add|mul|fma)_f32\b", text)
     assert not re.search(r"\bs_(store|buffer_store|atomic|dcache_wb)", text)
+
+
+# Memory instructions in the kernels are global (or LDS) ones: a flat access also counts against the
+# LDS wait counter, so every wait for an LDS read would wait for it too (a pointer rebuilt from an
+# integer loses its address space and turns a store into a flat store; the dS stores of the dK/dV
+# kernel cost a third more time that way).
+@pytest.mark.parametrize("src", ["fwd_bf16.hip", "bwd_bf16.hip", "bwd_bf16_d64.hip", "bwd_dq_bf16.hip",
+                                 "bwd_dq_bf16_d64.hip", "bwd_dq_ds.hip", "merge.hip", "bwd_pre.hip",
+                                 "tt_tokenize.hip"])
+def test_no_flat_memory_instructions(src, tmp_path):
+    text = _asm(src, tmp_path)
+    assert not re.search(r"^\s*flat_(load|store|atomic)", text, re.M)
 
 
 # The dK/dV kernel issues its matrix products as inline assembly (to choose the register file of
@@ -142,9 +154,10 @@ def test_hazard_check_catches_close_accesses():
     assert mfma_hazards(["v_accvgpr_write_b32 a2, v9", "s_nop 0", mfma])[1] == 1
 
 
-@pytest.mark.parametrize("src,kernel,products", [("bwd_bf16.hip", "bwd_dkdv_kernel", 80),
-                                                  ("bwd_dq_bf16.hip", "bwd_dq_kernel", 128)])
-def test_inline_mfma_spacing(src, kernel, products, tmp_path):
+# bwd_bf16.hip holds two d = 128 instances of the dK/dV kernel (with and without the dS stores)
+@pytest.mark.parametrize("src,kernel,products,count", [("bwd_bf16.hip", "bwd_dkdv_kernel", 80, 2),
+                                                        ("bwd_dq_bf16.hip", "bwd_dq_kernel", 128, 1)])
+def test_inline_mfma_spacing(src, kernel, products, count, tmp_path):
     text = _asm(src, tmp_path)
     # no register spills: these schedules keep every value in registers (a spill would add scratch
     # memory traffic the schedule does not account for)
@@ -152,7 +165,7 @@ def test_inline_mfma_spacing(src, kernel, products, tmp_path):
     assert sizes and all(int(x) == 0 for x in sizes), sizes
     bodies = _kernel_bodies(text)
     kernels = [(name, code) for name, code in bodies if kernel in name]
-    assert len(kernels) == 1, [n for n, _ in bodies]          # d = 128
+    assert len(kernels) == count, [n for n, _ in bodies]      # d = 128
     for name, code in kernels:
         assert sum(1 for c in code if c.startswith("v_mfma")) >= products, name
         near_result, near_write = mfma_hazards(code)
