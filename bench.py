@@ -341,9 +341,9 @@ def other_shapes(torch, np, inputs, ringx, stream, dev):
 # rocprofv3 outputs -> profiles/ summaries (CPU only; the commands that make the outputs are written
 # into each summary)
 
-PROFILE_STEP = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ring --no-gqa "
+PROFILE_STEP = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ring --no-gqa --no-stored-ds "
                 "--no-tokenizer --no-shapes --no-sclk")
-PROFILE_TRACE = ("python -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-ring --no-gqa "
+PROFILE_TRACE = ("python -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-ring --no-gqa --no-stored-ds "
                  "--no-tokenizer --no-shapes --no-sclk")
 BUSY_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CYCLES "
                  "SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS GRBM_GUI_ACTIVE")
@@ -354,7 +354,10 @@ PROFILE_KERNELS = [
      ["fwd_bf16.hip", "ringx_device.h"]),
     ("fwd_bf16_kernelILi128ELi1E", "fwd_bf16_kernel<128, partials>", "fwd_bf16_partials",
      ["fwd_bf16.hip", "ringx_device.h"]),
-    ("bwd_dkdv_kernelILi128E", "bwd_dkdv_kernel<128>", "bwd_dkdv", ["bwd_bf16.hip", "ringx_device.h"]),
+    ("bwd_dkdv_kernelILi128ELb0E", "bwd_dkdv_kernel<128>", "bwd_dkdv", ["bwd_bf16.hip", "ringx_device.h"]),
+    ("bwd_dkdv_kernelILi128ELb1E", "bwd_dkdv_kernel<128, dS stores>", "bwd_dkdv_store",
+     ["bwd_bf16.hip", "ringx_device.h"]),
+    ("bwd_dq_ds_kernel", "bwd_dq_ds_kernel", "bwd_dq_ds", ["bwd_dq_ds.hip", "ringx_device.h"]),
     ("bwd_dq_kernelILi128E", "bwd_dq_kernel<128>", "bwd_dq", ["bwd_dq_bf16.hip", "ringx_device.h"]),
     ("bwd_pre_bf16_kernelILi128E", "bwd_pre_bf16_kernel<128>", "bwd_pre", ["bwd_pre.hip", "ringx_device.h"]),
     ("merge_vec4_kernelILb1E", "merge_vec4_kernel<bf16 out>", "lse_merge", ["merge.hip", "ringx_device.h"]),
@@ -363,8 +366,8 @@ PROFILE_KERNELS = [
 
 def _profile_kernel(name):
     """rocprofv3 prints some names mangled and some demangled: match either form."""
-    demangled = {"ILi128ELi0E": "<128, 0>", "ILi128ELi1E": "<128, 1>", "ILi128E": "<128>",
-                 "ILb1E": "<true>"}
+    demangled = {"ILi128ELi0E": "<128, 0>", "ILi128ELi1E": "<128, 1>", "ILi128ELb0E": "<128, false>",
+                 "ILi128ELb1E": "<128, true>", "ILi128E": "<128>", "ILb1E": "<true>"}
     for frag, label, key, files in PROFILE_KERNELS:
         if frag in name:
             return label, key, files
@@ -572,6 +575,8 @@ def main():
                     help="skip the grouped-query measurement (H/4 K/V heads)")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the ring-step measurement (chunks arriving on a second stream)")
+    ap.add_argument("--no-stored-ds", action="store_true",
+                    help="skip the step with the backward through stored dS")
     ap.add_argument("--no-shapes", action="store_true",
                     help="skip the other paper-shaped workloads (16k single shard, turbulence "
                          "tokens, 524k long step)")
@@ -682,6 +687,7 @@ def main():
         f"pre {pre_ms:.3f} + dkdv {dkdv_ms:.2f} + dq {dq_ms:.2f}; wall {wall * 1e3 / K:.2f})")
     if not (torch.isfinite(out.float()).all() and torch.isfinite(dq).all()):
         raise RuntimeError("non-finite results")
+    dq_step = dq.clone()      # the other measurements below reuse dq
 
     U = w.gemm_unit()                      # 2*B*H*Nq*Nk*d
     value = 6 * U / (ms_step * 1e-3) / 1e12
@@ -808,6 +814,68 @@ def main():
                                 "what": "fwd+bwd with H/4 K/V heads (grouped-query attention)"}
         log(f"[bench] gqa (Hkv={hkv}): {gms:.2f} ms/step, {6 * U / (gms * 1e-3) / 1e12:.1f} TFLOP/s")
         del kg, vg, dkg, dvg
+
+    # the same step with the backward through stored dS (ringx_attn_bwd_ds as its stages): the
+    # dK/dV kernel also writes every bf16 dS, and dQ is streamed from them (7U executed instead of
+    # 9U), in slabs of two K/V heads (2 B H Nq Nk / (B H) * 2 bytes of workspace)
+    if not args.no_stored_ds and d == 128 and B * H >= 2:
+        slab = 2
+        ds_buf = torch.empty(ringx.ringx_bwd_ds_bytes(H, H, Nq, Nk, d, R, slab), dtype=torch.uint8,
+                             device=dev)
+        dq_s = torch.empty_like(dq)
+        nslab = (B * H + slab - 1) // slab
+
+        def stored_step(marks=None):
+            m = marks or [None] * (2 + 2 * nslab)
+            if m[0]: m[0].record(stream)
+            ringx.ringx_attn_fwd(q, k, v, R, scale=w.scale, out=out, lse=lse, stream=stream)
+            ringx.ringx_bwd_preprocess(out, do, lse, delta=delta, stream=stream)
+            for i in range(nslab):
+                kv0, n = i * slab, min(slab, B * H - i * slab)
+                if m[1 + 2 * i]: m[1 + 2 * i].record(stream)
+                ringx.ringx_attn_bwd_dkdv_ds(q, k, v, do, lse, delta, R, ds_buf, kv0, n,
+                                             scale=w.scale, dk=dk, dv=dv, stream=stream)
+                if m[2 + 2 * i]: m[2 + 2 * i].record(stream)
+                ringx.ringx_attn_bwd_dq_ds(ds_buf, k, (B, H, Nq, d), R, kv0, n, scale=w.scale,
+                                           dq=dq_s, stream=stream)
+            if m[-1]: m[-1].record(stream)
+
+        stored_step()
+        torch.cuda.synchronize()
+        ns = max(1, min(K, 3))
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2 + 2 * nslab)]
+               for _ in range(ns)]
+        for i in range(ns):
+            stored_step(evs[i])
+        torch.cuda.synchronize()
+        sms = sum(e[0].elapsed_time(e[-1]) for e in evs) / ns
+        s_dkdv = sum(e[1 + 2 * i].elapsed_time(e[2 + 2 * i]) for e in evs
+                     for i in range(nslab)) / ns
+        s_dq = sum(e[2 + 2 * i].elapsed_time(e[3 + 2 * i] if 3 + 2 * i < len(e) - 1 else e[-1])
+                   for e in evs for i in range(nslab)) / ns
+        ds_total = ringx.ringx_bwd_ds_bytes(H, H, Nq, Nk, d, R, B * H)
+        # the dQ pass reads every stored dS once, K once per head, and writes dq
+        dq_bytes = ds_total + B * H * Nk * d * 2 + B * H * Nq * d * 4
+        kernels["stored_ds_steps"] = {
+            "ms": sms, "steps": ns, "slab_heads": slab, "workspace_bytes": int(ds_buf.numel()),
+            "tflops": 6 * U / (sms * 1e-3) / 1e12,
+            "vs_recompute_step": sms / ms_step - 1.0,
+            "bwd_dkdv_kernel_store": {"ms": s_dkdv, "executed_tflops": tf(4 * U, s_dkdv),
+                                      "ds_bytes_written": ds_total,
+                                      "GB/s_written": ds_total / (s_dkdv * 1e-3) / 1e9},
+            "bwd_dq_ds_kernel": {"ms": s_dq, "bytes": dq_bytes, "executed_tflops": tf(U, s_dq),
+                                 "GB/s": dq_bytes / (s_dq * 1e-3) / 1e9,
+                                 "frac": dq_bytes / (s_dq * 1e-3) / 1e9 / PEAK_HBM_GBS},
+            "what": "fwd + bwd with dS stored by the dK/dV pass and dQ streamed from it "
+                    "(7U of matrix products executed instead of 9U)",
+        }
+        rq = float(((dq_s - dq_step).double().pow(2).mean().sqrt() /
+                    dq_step.double().pow(2).mean().sqrt()))
+        kernels["stored_ds_steps"]["dq_rel_rms_vs_recompute"] = rq
+        log(f"[bench] stored dS: {sms:.2f} ms/step ({100 * (sms / ms_step - 1):+.1f}% vs recompute;"
+            f" dkdv+store {s_dkdv:.2f}, dq from dS {s_dq:.2f} ms = "
+            f"{dq_bytes / (s_dq * 1e-3) / 1e12:.2f} TB/s)")
+        del ds_buf, dq_s
 
     # multi-fidelity tokenizer: the three fidelity modes of Table III's (filter, ratio) pairs
     # (1, 8x), (4, 2x), (8, 1x) with patch 1 over a DNS-sized 1024^3 x 4 fp32 field
