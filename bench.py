@@ -345,6 +345,9 @@ PROFILE_STEP = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-
                 "--no-tokenizer --no-shapes --no-sclk")
 PROFILE_TRACE = ("python -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-ring --no-gqa --no-stored-ds "
                  "--no-tokenizer --no-shapes --no-sclk")
+# the step with the backward through stored dS (run once after one plain step)
+PROFILE_DS = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ring --no-gqa "
+              "--no-merge --no-tokenizer --no-shapes --no-sclk")
 BUSY_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CYCLES "
                  "SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS GRBM_GUI_ACTIVE")
 
@@ -544,6 +547,7 @@ def summarize_profiles(root, workload):
            "bench.py for the two backward kernels."]
     with open(os.path.join(prof, f"mfma_busy_{workload}.md"), "w") as f:
         f.write("\n".join(md) + "\n")
+    _summarize_stored_ds(root, workload, w, shape, prof, cmd, ff, wf)
     # the bench line of a plain `python bench.py` run beside the profiles, if there is one
     full = os.path.join(root, "bench.json")
     if os.path.exists(full):
@@ -555,6 +559,69 @@ def summarize_profiles(root, workload):
             json.dump(bench_line, f, indent=1)
             f.write("\n")
     print(f"wrote summaries of {root} under profiles/")
+
+
+def _summarize_stored_ds(root, workload, w, shape, prof, cmd, ff, wf):
+    """Kernel trace and HBM counters of the step with the backward through stored dS, when the
+    three runs are there (trace, FETCH_SIZE, WRITE_SIZE of PROFILE_DS)."""
+    tdir = os.path.join(root, "prof_trace_ds")
+    if not os.path.isdir(tdir):
+        return
+    from paper_2507_16697_amd import ringx
+    B, H, Nq, Nk, d, R = w.B, w.H, w.Nq, w.Nk, w.d, w.R
+    stats = _read_csv(os.path.join(tdir, "ring8ds_kernel_stats.csv"))
+    lines = []
+    for r in stats:
+        k = _profile_kernel(r["Name"])
+        if k:
+            lines.append((k[0], k[1], int(r["Calls"]), float(r["AverageNs"]), float(r["MinNs"]),
+                          float(r["MaxNs"])))
+    lines.sort(key=lambda x: -x[3] * x[2])
+    slab = 2
+    ds_slab = ringx.ringx_bwd_ds_bytes(H, H, Nq, Nk, d, R, slab)
+    alg = {  # bytes per launch (one slab of two heads) that each kernel must move at least
+        "bwd_dkdv_store": (2 * slab * Nk * d * 2 + 2 * slab * Nq * d * 2 + 2 * slab * Nq * 4,
+                           ds_slab + 2 * slab * Nk * d * 4),
+        "bwd_dq_ds": (ds_slab + slab * Nk * d * 2, slab * Nq * d * 4),
+    }
+    fetch = _pmc_per_dispatch(os.path.join(root, "pmc_ds_FETCH_SIZE"), "FETCH_SIZE") \
+        if os.path.isdir(os.path.join(root, "pmc_ds_FETCH_SIZE")) else {}
+    write = _pmc_per_dispatch(os.path.join(root, "pmc_ds_WRITE_SIZE"), "WRITE_SIZE") \
+        if os.path.isdir(os.path.join(root, "pmc_ds_WRITE_SIZE")) else {}
+    per = {}
+    for src, which in ((fetch, 0), (write, 1)):
+        for _, (name, val) in src.items():
+            k = _profile_kernel(name)
+            if k and k[1] in alg:
+                per.setdefault(k[1], ([], []))[which].append(val)
+    md = [f"# Backward through stored dS: {workload} ({shape})", "",
+          "Commands (run from the repository root on one MI355X):", "",
+          "    " + cmd("prof_trace_ds", "ring8ds", "--kernel-trace --stats") + PROFILE_DS,
+          "    " + cmd("pmc_ds_FETCH_SIZE", "pmc", "--pmc FETCH_SIZE") + PROFILE_DS,
+          "    " + cmd("pmc_ds_WRITE_SIZE", "pmc", "--pmc WRITE_SIZE") + PROFILE_DS, "",
+          "Each run makes one plain step and two steps through stored dS (one untimed), each of "
+          f"those a forward, a preprocess and {B * H // slab} slabs of {slab} heads (dK/dV with the "
+          "dS stores, then dQ from the stored dS).  Durations in ns; only libringx kernels.", "",
+          "| kernel | calls | average ns | min ns | max ns | total ms per step |",
+          "|---|---|---|---|---|---|"]
+    nsteps = {"bwd_dkdv_store": 2, "bwd_dq_ds": 2}
+    for label, key, c, avg, mn, mx in lines:
+        per_step = (c / nsteps[key] * avg / 1e6) if key in nsteps else float("nan")
+        md.append(f"| {label} | {c} | {avg:.0f} | {mn:.0f} | {mx:.0f} | "
+                  + (f"{per_step:.2f} |" if key in nsteps else "- |"))
+    if per:
+        md += ["", "HBM bytes per launch (one slab of two heads), counters calibrated as in "
+               f"hbm_traffic_{workload}.md (fetched = FETCH_SIZE x 1024 x {ff:.4f}, written = "
+               f"WRITE_SIZE x 1024 x {wf:.4f}), against the bytes the kernel must move:", "",
+               "| kernel | fetched GB | algorithmic read GB | written GB | algorithmic write GB |",
+               "|---|---|---|---|---|"]
+        for key, (fv, wv) in per.items():
+            fb = sorted(fv)[len(fv) // 2] * 1024 * ff if fv else float("nan")
+            wb = sorted(wv)[len(wv) // 2] * 1024 * wf if wv else float("nan")
+            md.append(f"| {key} | {fb / 1e9:.2f} | {alg[key][0] / 1e9:.2f} | {wb / 1e9:.2f} | "
+                      f"{alg[key][1] / 1e9:.2f} |")
+    with open(os.path.join(prof, f"kernel_trace_stored_ds_{workload}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
 
 
 def main():
