@@ -50,7 +50,6 @@ struct DqsCfg {
   static constexpr int kLds = kStages * kStage;
   static constexpr int kLoads = kTile / (kThreads * 16);     // K loads per thread per tile
   static constexpr int kDsLoads = kDsTile / (kThreads * 16); // dS loads per thread per tile
-  static constexpr int kTileOps = kLoads + kDsLoads;
   static constexpr int kCT = D / 32;
   static_assert(kTile == kLoads * kThreads * 16 && kDsTile == kDsLoads * kThreads * 16, "loads");
   static_assert(kDsTile == 8 * kDsUnitBytes, "a tile is two key blocks of four units");
