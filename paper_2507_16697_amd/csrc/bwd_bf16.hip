@@ -25,7 +25,9 @@
 // loads three tiles ahead; one barrier per tile.  Rows past Nq in a head's last tile are clamped
 // copies whose dO row and D are zeroed in LDS, so they add nothing; key lanes past the chunk end
 // only feed their own dK/dV columns, which are not written.  dQ is computed by the
-// query-stationary kernel in bwd_dq_bf16.hip.
+// query-stationary kernel in bwd_dq_bf16.hip, or, in store mode (kStore), from the -dS operands
+// this kernel writes out (bwd_dq_ds.hip): 4 KiB per wave and tile, two 1 KiB global stores per
+// 32-query block.
 //
 // Register files: the 128 dK^T/dV^T accumulators and the K/V fragments live in AGPRs (MFMA
 // accumulator and operand registers), the S/dP accumulators, P/dS and the operands in flight in
