@@ -426,6 +426,12 @@ def summarize_profiles(root, workload):
             lines.append((k[0], int(r["Calls"]), float(r["AverageNs"]), float(r["MinNs"]),
                           float(r["MaxNs"])))
     lines.sort(key=lambda x: -x[2])
+    # dispatches per call of each entry point (dK/dV is launched two K/V heads at a time): the
+    # trace's calls over the fused forward's, one of which runs per step
+    calls_of = {lab: c for lab, c, _, _, _ in lines}
+    per_step = calls_of.get("fwd_bf16_kernel<128, fused merge>", 1) or 1
+    per_call = {lab: max(1, round(c / per_step)) for lab, c, _, _, _ in lines
+                if lab.startswith("bwd_dkdv")}
     bench_line = None
     log_path = os.path.join(root, "prof_trace.log")
     if os.path.exists(log_path):
@@ -437,9 +443,12 @@ def summarize_profiles(root, workload):
           "    " + cmd("prof_trace", "ring8", "--kernel-trace --stats") + PROFILE_TRACE, "",
           "The run makes 4 forward and 4 backward passes (1 warmup + 3 timed; each backward = "
           "preprocess + dK/dV + dQ), 1 partials forward and 11 standalone merges.  Durations in ns; "
-          "only libringx kernels are listed.", "",
-          "| kernel | calls | average ns | min ns | max ns |", "|---|---|---|---|---|"]
-    md += [f"| {a} | {c} | {avg:.0f} | {mn:.0f} | {mx:.0f} |" for a, c, avg, mn, mx in lines]
+          "only libringx kernels are listed.  A call of ringx_attn_bwd_dkdv launches its kernel "
+          "once per two K/V heads; the last column is the time per call.", "",
+          "| kernel | dispatches | average ns per dispatch | min ns | max ns | dispatches per call "
+          "| ms per call |", "|---|---|---|---|---|---|---|"]
+    md += [f"| {a} | {c} | {avg:.0f} | {mn:.0f} | {mx:.0f} | {per_call.get(a, 1)} | "
+           f"{avg * per_call.get(a, 1) / 1e6:.2f} |" for a, c, avg, mn, mx in lines]
     if bench_line:
         c = bench_line["config"]
         md += ["", f"bench.py in the same run (HIP events around each call, "
@@ -480,7 +489,8 @@ def summarize_profiles(root, workload):
             cmd("pmc_WRITE_SIZE", "pmc", "--pmc WRITE_SIZE") + PROFILE_STEP,
             cmd("pmc_copy_FETCH_SIZE", "pmc", "--pmc FETCH_SIZE") + "python -u bench.py --copy-probe",
             cmd("pmc_copy_WRITE_SIZE", "pmc", "--pmc WRITE_SIZE") + "python -u bench.py --copy-probe"]
-    md = [f"# HBM traffic per launch: {workload} ({shape})", "",
+    label_of = {key: lab for _, lab, key, _ in PROFILE_KERNELS}
+    md = [f"# HBM traffic per call: {workload} ({shape})", "",
           "Counters: `FETCH_SIZE` and `WRITE_SIZE` (KiB per dispatch, L2-to-fabric traffic, so reads "
           "served by", "the MALL count as fetched), each in a run of its own:", ""]
     md += ["    " + c for c in cmds[:2]]
@@ -488,15 +498,17 @@ def summarize_profiles(root, workload):
            "3 copies):", ""] + ["    " + c for c in cmds[2:]]
     md += ["", f"The copy reads 1 GiB and writes 1 GiB; FETCH_SIZE reports {cf_kib:.0f} KiB and "
            f"WRITE_SIZE {cw_kib:.0f} KiB, so fetched bytes = FETCH_SIZE x 1024 x {ff:.4f} and written "
-           f"bytes = WRITE_SIZE x 1024 x {wf:.4f}.", "",
+           f"bytes = WRITE_SIZE x 1024 x {wf:.4f}.  Per call: the median dispatch times the "
+           "dispatches per call (dK/dV: one per two K/V heads).", "",
            "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | fetched GB | written GB | traffic GB | "
            "algorithmic GB | traffic / algorithmic |", "|---|---|---|---|---|---|---|---|"]
     for key in ("fwd_bf16", "fwd_bf16_partials", "bwd_dkdv", "bwd_dq", "bwd_pre", "lse_merge"):
         if key not in per_kernel:
             continue
         fv, wv, files = per_kernel[key]
-        fk = sorted(fv)[len(fv) // 2]
-        wk = sorted(wv)[len(wv) // 2] if wv else 0.0
+        npc = per_call.get(label_of.get(key), 1)
+        fk = sorted(fv)[len(fv) // 2] * npc
+        wk = (sorted(wv)[len(wv) // 2] if wv else 0.0) * npc
         fb, wb = fk * 1024 * ff, wk * 1024 * wf
         md.append(f"| {key} | {fk:.0f} | {wk:.0f} | {fb / 1e9:.3f} | {wb / 1e9:.3f} | "
                   f"{(fb + wb) / 1e9:.3f} | {alg[key] / 1e9:.3f} | {(fb + wb) / alg[key]:.2f} |")
@@ -534,14 +546,24 @@ def summarize_profiles(root, workload):
           "rate the", "matrix cores deliver is MFMA busy x clock / 2.4 GHz x 2516.6 TFLOP/s.", "",
           "| kernel | duration ms | clock GHz | MFMA busy | MFMA co-issue | delivered TFLOP/s | LDS "
           "busy | LDS bank conflicts | LDS instructions |", "|---|---|---|---|---|---|---|---|---|"]
-    seen = set()
+    # the first call of each kernel: its dispatches' durations and counters summed
+    first = {}
     for did in sorted(disp):
         e = disp[did]
         k = _profile_kernel(e["name"])
-        if not k or k[0] in seen:
+        if not k:
             continue
-        seen.add(k[0])
-        ms = (e["t1"] - e["t0"]) * 1e-6
+        agg = first.setdefault(k[0], {"n": 0, "ms": 0.0})
+        if agg["n"] >= per_call.get(k[0], 1):
+            continue
+        agg["n"] += 1
+        agg["ms"] += (e["t1"] - e["t0"]) * 1e-6
+        for cname, val in e.items():
+            if cname.startswith(("SQ_", "GRBM_")):
+                agg[cname] = agg.get(cname, 0.0) + val
+    for lab, e in first.items():
+        k = (lab,)
+        ms = e["ms"]
         cyc = e.get("GRBM_GUI_ACTIVE", 0.0) / 8
         ghz = cyc / (ms * 1e6) if ms > 0 else 0.0
         busy = e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (cyc * 1024) if cyc else 0.0

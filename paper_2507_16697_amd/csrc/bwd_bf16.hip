@@ -527,13 +527,29 @@ hipError_t launch(const BwdArgs& a) {
   const int64_t max_chunk = (a.Nk + a.R - 1) / a.R;
   const int64_t tpc = (max_chunk + C::kBK - 1) / C::kBK;
   static_assert(C::kBK == 128, "stored-dS layout: 128-key tiles");
-  const int64_t nwg = a.BH / a.G * a.R * tpc;
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, kStore>), dim3((uint32_t)nwg), dim3(C::kThreads), 0,
-                     a.stream, (const __bf16*)a.q, (const __bf16*)a.k, (const __bf16*)a.v,
-                     (const __bf16*)a.dout, a.nl, a.delta, a.dk, a.dv, (int)(a.BH / a.G),
-                     (int)a.H, (int)a.G, a.Nq, a.Nk, (int)a.R, (int)tpc, a.scale * kLog2e,
-                     a.scale, a.accumulate_dkv ? 1 : 0, a.ds);
-  return hipGetLastError();
+  const int64_t bhkv = a.BH / a.G;
+  // Two K/V heads per launch (store mode: the caller's slab).  The workgroups of an XCD sweep a
+  // head's queries together, each tile fetched from HBM once per XCD and round only while they
+  // stay in step; over the 128 rounds of a whole-tensor launch they drift apart and fetch 25-70 GB
+  // instead of the 20 GB of launches that each end after 16 rounds, at the same speed.
+  const int64_t per_launch = kStore ? bhkv : 2;
+  for (int64_t h0 = 0; h0 < bhkv; h0 += per_launch) {
+    const int64_t nh = bhkv - h0 < per_launch ? bhkv - h0 : per_launch;
+    // K/V head m serves query heads m G .. m G + G - 1: one launch is a batch of nh K/V heads
+    // with G query heads each
+    const int64_t q0 = h0 * a.G;
+    const int64_t nwg = nh * a.R * tpc;
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, kStore>), dim3((uint32_t)nwg), dim3(C::kThreads), 0,
+                       a.stream, (const __bf16*)a.q + q0 * a.Nq * D,
+                       (const __bf16*)a.k + h0 * a.Nk * D, (const __bf16*)a.v + h0 * a.Nk * D,
+                       (const __bf16*)a.dout + q0 * a.Nq * D, a.nl + q0 * a.Nq,
+                       a.delta + q0 * a.Nq, a.dk + h0 * a.Nk * D, a.dv + h0 * a.Nk * D, (int)nh,
+                       (int)a.G, (int)a.G, a.Nq, a.Nk, (int)a.R, (int)tpc, a.scale * kLog2e,
+                       a.scale, a.accumulate_dkv ? 1 : 0, a.ds);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
