@@ -827,6 +827,8 @@ def main():
         "kernel": dominant, "bound": "mfma", "achieved": dom["tflops"], "peak": PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s", "frac": dom["frac"], "traffic": dom["traffic"],
         "work_per_launch": f"{dom['flops']:.4e} flops = {dom['work']}",
+        # one call of ringx_attn_bwd_dkdv runs its kernel once per two K/V heads
+        "dispatches_per_call": -(-B * H // 2) if dominant == "bwd_dkdv_kernel" else 1,
     }
 
     # standalone Eq. (5) merge of the R per-chunk partials (an HBM-bound kernel)
