@@ -918,10 +918,13 @@ def main():
     # the same step with the backward through stored dS (ringx_attn_bwd_ds as its stages): the
     # dK/dV kernel also writes every bf16 dS, and dQ is streamed from them (7U executed instead of
     # 9U), in slabs of two K/V heads (2 B H Nq Nk / (B H) * 2 bytes of workspace)
-    if not args.no_stored_ds and d == 128 and B * H >= 2:
+    ds_need = ringx.ringx_bwd_ds_bytes(H, H, Nq, Nk, d, R, 2) if d == 128 and B * H >= 2 else 0
+    ds_fits = ds_need > 0 and torch.cuda.mem_get_info(dev)[0] > ds_need + (4 << 30)
+    if not args.no_stored_ds and ds_need and not ds_fits:
+        log(f"[bench] stored dS skipped: {ds_need / 2**30:.0f} GiB of workspace does not fit")
+    if not args.no_stored_ds and ds_fits:
         slab = 2
-        ds_buf = torch.empty(ringx.ringx_bwd_ds_bytes(H, H, Nq, Nk, d, R, slab), dtype=torch.uint8,
-                             device=dev)
+        ds_buf = torch.empty(ds_need, dtype=torch.uint8, device=dev)
         dq_s = torch.empty_like(dq)
         nslab = (B * H + slab - 1) // slab
 
