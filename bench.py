@@ -66,6 +66,14 @@ def load_traffic(kernel, workload, src_hash):
     return rec.get("bytes_per_launch")
 
 
+def _dkdv_dispatches(bhkv, Nk, R):
+    """Kernel launches per ringx_attn_bwd_dkdv call at d = 128 (the library's grouping of K/V
+    heads: about 4096 workgroups of 128 keys per launch)."""
+    tpc = -(-(-(-Nk // R)) // 128)
+    per = max(1, 4096 // (R * tpc))
+    return -(-bhkv // per)
+
+
 def _oracle_fwd_bwd(inputs, oracle, t, w, h, rows, with_bwd=True):
     """Seconds of the fp64 oracle, as it stands, on head h: queries 0..rows-1 against all keys,
     forward (+ backward).  Returns (seconds, flops of the 4 (+8) * rows * Nk * d convention)."""
@@ -827,8 +835,9 @@ def main():
         "kernel": dominant, "bound": "mfma", "achieved": dom["tflops"], "peak": PEAK_BF16_TFLOPS,
         "unit": "TFLOP/s", "frac": dom["frac"], "traffic": dom["traffic"],
         "work_per_launch": f"{dom['flops']:.4e} flops = {dom['work']}",
-        # one call of ringx_attn_bwd_dkdv runs its kernel once per two K/V heads
-        "dispatches_per_call": -(-B * H // 2) if dominant == "bwd_dkdv_kernel" else 1,
+        # one call of ringx_attn_bwd_dkdv runs its kernel on groups of K/V heads of about 16 rounds
+        # of 256 workgroups each (two heads at the 8-way ring share)
+        "dispatches_per_call": _dkdv_dispatches(B * H, Nk, R) if dominant == "bwd_dkdv_kernel" else 1,
     }
 
     # standalone Eq. (5) merge of the R per-chunk partials (an HBM-bound kernel)

@@ -40,6 +40,7 @@
 #include "ringx_device.h"
 #include "ringx_kernels.h"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace ringx {
@@ -528,11 +529,12 @@ hipError_t launch(const BwdArgs& a) {
   const int64_t tpc = (max_chunk + C::kBK - 1) / C::kBK;
   static_assert(C::kBK == 128, "stored-dS layout: 128-key tiles");
   const int64_t bhkv = a.BH / a.G;
-  // Two K/V heads per launch (store mode: the caller's slab).  The workgroups of an XCD sweep a
-  // head's queries together, each tile fetched from HBM once per XCD and round only while they
-  // stay in step; over the 128 rounds of a whole-tensor launch they drift apart and fetch 25-70 GB
-  // instead of the 20 GB of launches that each end after 16 rounds, at the same speed.
-  const int64_t per_launch = kStore ? bhkv : 2;
+  // About 16 rounds of 256 workgroups per launch (two K/V heads at the 8-way ring share; store
+  // mode: the caller's slab).  The workgroups of an XCD sweep a head's queries together, each tile
+  // fetched from HBM once per XCD and round only while they stay in step; over the 128 rounds of a
+  // whole-tensor launch they drift apart and fetch 25-76 GB instead of the 20 GB of launches that
+  // each end after 16 rounds, at the same speed.
+  const int64_t per_launch = kStore ? bhkv : std::max<int64_t>(1, 4096 / (a.R * tpc));
   for (int64_t h0 = 0; h0 < bhkv; h0 += per_launch) {
     const int64_t nh = bhkv - h0 < per_launch ? bhkv - h0 : per_launch;
     // K/V head m serves query heads m G .. m G + G - 1: one launch is a batch of nh K/V heads
