@@ -328,6 +328,36 @@ def test_backward_stages_compose(dtype, d):
     assert max_abs_err(to_host_f64(delta[1]), ref_nl) <= 2.0 ** -22 * max(1.0, float(np.abs(ref_nl).max()))
 
 
+@pytest.mark.parametrize("H,Hkv", [(3, 3), (6, 3)])
+def test_dkdv_launch_groups_match_per_head_calls(H, Hkv):
+    """At a key length where ringx_attn_bwd_dkdv splits its launch into groups of K/V heads (two
+    per launch at 262,144 keys in 8 chunks, the last group ragged), the gradients equal those of
+    one call per K/V head (each a single launch) bitwise: the groups only move pointers."""
+    B, Nq, Nk, d, R = 1, 128, 262144, 128, 8
+    G = H // Hkv
+    q = inputs.make_iid(B, H, Nq, 1, d, seed=31, std=2 ** -0.5, store="bf16", do_std=2 ** -0.5)
+    kv = inputs.make_iid(B, Hkv, 1, Nk, d, seed=32, std=2 ** -0.5, store="bf16", with_do=False)
+    g = {"q": to_device(q["q"], "bf16"), "do": to_device(q["do"], "bf16"),
+         "k": to_device(kv["k"], "bf16"), "v": to_device(kv["v"], "bf16")}
+    out, lse = ringx.ringx_attn_fwd_gqa(g["q"], g["k"], g["v"], R)
+    delta = ringx.ringx_bwd_preprocess(out, g["do"], lse)
+    if Hkv == H:
+        dk, dv = ringx.ringx_attn_bwd_dkdv(g["q"], g["k"], g["v"], g["do"], lse, delta, R)
+    else:
+        _, dk, dv = ringx.ringx_attn_bwd_gqa(g["q"], g["k"], g["v"], out, g["do"], lse, R)
+    for m in range(Hkv):
+        hs = slice(m * G, (m + 1) * G)
+        dl = delta[:, :, hs].contiguous()
+        qs, dos, ls = g["q"][:, hs], g["do"][:, hs], lse[:, hs]
+        ks, vs = g["k"][:, m:m + 1], g["v"][:, m:m + 1]
+        if G == 1:
+            dk1, dv1 = ringx.ringx_attn_bwd_dkdv(qs, ks, vs, dos, ls, dl, R)
+        else:
+            _, dk1, dv1 = ringx.ringx_attn_bwd_gqa(qs, ks, vs, out[:, hs], dos, ls, R)
+        torch.cuda.synchronize()
+        assert torch.equal(dk1[:, 0], dk[:, m]) and torch.equal(dv1[:, 0], dv[:, m]), m
+
+
 def test_errors_leave_outputs_untouched():
     q = torch.randn((1, 1, 16, 64), device="cuda").to(torch.bfloat16)
     k = torch.randn((1, 1, 8, 64), device="cuda").to(torch.bfloat16)
