@@ -1002,12 +1002,16 @@ def main():
             tok = ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, stream=stream)
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            # the (1, 8x) crop runs for about 14 us, less than the binding takes to enqueue a
+            # call: a spin kernel holds the stream until all calls are queued, so that the
+            # events time the kernels back to back rather than the host's launch rate
+            torch.cuda._sleep(20_000_000)
             e0.record(stream)
-            for _ in range(5):
+            for _ in range(20):
                 ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, tokens=tok, stream=stream)
             e1.record(stream)
             torch.cuda.synchronize()
-            tms = e0.elapsed_time(e1) / 5
+            tms = e0.elapsed_time(e1) / 20
             nbytes = C_ * (D_ // ratio) ** 3 * 4 + tok.numel() * 4
             modes.append({"filter": k_, "ratio": ratio, "tokens": tok.shape[0], "ms": tms,
                           "bytes": nbytes, "GB/s": nbytes / (tms * 1e-3) / 1e9,
