@@ -367,6 +367,23 @@ PROFILE_DS = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ri
               "--no-merge --no-tokenizer --no-shapes --no-sclk")
 BUSY_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CYCLES "
                  "SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS GRBM_GUI_ACTIVE")
+# instruction mix and wave states of every matrix kernel of the step and the other shapes (two
+# counter passes: at most 8 SQ counters per run)
+PROFILE_MIX = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ring --no-gqa "
+               "--no-stored-ds --no-tokenizer --no-sclk --no-merge")
+MIX_COUNTERS = [("pmc_stall1", "SQ_WAVE_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS "
+                 "SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_ANY SQ_ACTIVE_INST_MISC "
+                 "GRBM_GUI_ACTIVE"),
+                ("pmc_stall2", "SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS SQ_INSTS_SALU "
+                 "SQ_INSTS_VALU_TRANS_F32 SQ_BUSY_CYCLES SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VMEM "
+                 "GRBM_GUI_ACTIVE")]
+# matrix kernels of the instruction-mix summary: mangled fragment -> label, waves per SIMD
+MIX_KERNELS = [("fwd_bf16_kernelILi128ELi0E", "fwd_bf16_kernel<128, fused merge>", 2),
+               ("bwd_dkdv_kernelILi128ELb0E", "bwd_dkdv_kernel<128>", 1),
+               ("bwd_dq_kernelILi128E", "bwd_dq_kernel<128>", 1),
+               ("fwd_bf16_kernelILi64ELi0E", "fwd_bf16_kernel<64, fused merge>", 2),
+               ("bwd_dkdv_kernelILi64E", "bwd_dkdv_kernel<64>", 2),
+               ("bwd_dq_kernelILi64E", "bwd_dq_kernel<64>", 2)]
 
 # mangled-name fragment -> (label in the summaries, traffic key, source files of its hash)
 PROFILE_KERNELS = [
@@ -587,6 +604,7 @@ def summarize_profiles(root, workload):
     with open(os.path.join(prof, f"mfma_busy_{workload}.md"), "w") as f:
         f.write("\n".join(md) + "\n")
     _summarize_stored_ds(root, workload, w, shape, prof, cmd, ff, wf)
+    _summarize_instruction_mix(root, workload, prof, cmd)
     # the bench line of a plain `python bench.py` run beside the profiles, if there is one
     full = os.path.join(root, "bench.json")
     if os.path.exists(full):
@@ -598,6 +616,58 @@ def summarize_profiles(root, workload):
             json.dump(bench_line, f, indent=1)
             f.write("\n")
     print(f"wrote summaries of {root} under profiles/")
+
+
+def _summarize_instruction_mix(root, workload, prof, cmd):
+    """Instructions per matrix product and wave states of each matrix kernel, summed over all its
+    dispatches in the two MIX_COUNTERS passes (when both are there)."""
+    paths = [os.path.join(root, d_, "pmc_counter_collection.csv") for d_, _ in MIX_COUNTERS]
+    if not all(os.path.exists(p) for p in paths):
+        return
+    tot = {}
+    for p in paths:
+        for r in _read_csv(p):
+            name = r["Kernel_Name"]
+            for frag, label, wps in MIX_KERNELS:
+                if frag in name:
+                    e = tot.setdefault(label, {"wps": wps, "disp": set()})
+                    e["disp"].add((p, int(r["Dispatch_Id"])))
+                    e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                    break
+    md = [f"# Instruction mix and wave states of the matrix kernels: {workload} and the other "
+          "shapes", "", "Commands (run from the repository root on one MI355X, one counter pass "
+          "each; the run also makes the", "16k single shard and turbulence-token passes at d = 64 "
+          "and the 524k long step):", ""]
+    md += ["    " + cmd(d_, "pmc", "--pmc " + c) + PROFILE_MIX for d_, c in MIX_COUNTERS]
+    md += ["", "Per matrix product (v_mfma_f32_32x32x16_bf16, 32 cycles of a SIMD's matrix core): "
+           "vector-ALU", "instructions other than the products (SQ_INSTS_VALU - SQ_INSTS_MFMA), of "
+           "them transcendental", "(SQ_INSTS_VALU_TRANS_F32: the exponentials), LDS and scalar "
+           "instructions (s_waitcnt included).", "Wave states as fractions of SQ_WAVE_CYCLES: "
+           "waiting on a counter or barrier (SQ_WAIT_ANY), ready but", "not issued (SQ_WAIT_INST_ANY), "
+           "issuing vector-ALU (SQ_ACTIVE_INST_VALU, products included) and LDS", "instructions "
+           "(SQ_ACTIVE_INST_LDS).  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x "
+           "1024).", "",
+           "| kernel | waves per SIMD | dispatches | VALU / product | exp / product | LDS / product "
+           "| scalar / product | MFMA busy | waiting | not issued | VALU active | LDS active |",
+           "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for _, label, _ in MIX_KERNELS:
+        e = tot.get(label)
+        if not e or not e.get("SQ_INSTS_MFMA") or not e.get("SQ_WAVE_CYCLES"):
+            continue
+        m, wc = e["SQ_INSTS_MFMA"], e["SQ_WAVE_CYCLES"]
+        # GRBM_GUI_ACTIVE is in both passes: the matrix-core busy fraction uses the second's
+        cyc = sum(float(r["Counter_Value"]) for r in _read_csv(paths[1])
+                  if r["Counter_Name"] == "GRBM_GUI_ACTIVE"
+                  and any(f in r["Kernel_Name"] for f, lab, _ in MIX_KERNELS if lab == label)) / 8
+        busy = e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (cyc * 1024) if cyc else 0.0
+        md.append(f"| {label} | {e['wps']} | {len(e['disp']) // 2} | "
+                  f"{(e['SQ_INSTS_VALU'] - m) / m:.2f} | {e['SQ_INSTS_VALU_TRANS_F32'] / m:.2f} | "
+                  f"{e['SQ_INSTS_LDS'] / m:.2f} | {e['SQ_INSTS_SALU'] / m:.2f} | {100 * busy:.1f}% | "
+                  f"{100 * e['SQ_WAIT_ANY'] / wc:.1f}% | {100 * e['SQ_WAIT_INST_ANY'] / wc:.1f}% | "
+                  f"{100 * e['SQ_ACTIVE_INST_VALU'] / wc:.1f}% | "
+                  f"{100 * e['SQ_ACTIVE_INST_LDS'] / wc:.1f}% |")
+    with open(os.path.join(prof, f"instruction_mix_{workload}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
 
 
 def _summarize_stored_ds(root, workload, w, shape, prof, cmd, ff, wf):
@@ -694,7 +764,8 @@ def main():
                          "the GPU)")
     ap.add_argument("--profile-summary", metavar="DIR",
                     help="CPU only: turn the rocprofv3 outputs under DIR (prof_trace, pmc_FETCH_SIZE, "
-                         "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE, pmc_busy) into "
+                         "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE, pmc_busy; pmc_stall1 and "
+                         "pmc_stall2 when present) into "
                          "the summaries under profiles/")
     args = ap.parse_args()
     if args.profile_summary:
