@@ -61,6 +61,7 @@ typedef enum ringx_status RINGX_ENUM_BASE {
   RINGX_OK = 0,
   RINGX_E_NULLPTR = 1,     /* a required pointer is NULL                                     */
   RINGX_E_SHAPE = 2,       /* B, H, Nq, Nk < 1, a size overflows, or scale not finite and > 0 */
+                           /* (also Nk > 2^31 or Nq > 2^31 - 128 per head)                   */
   RINGX_E_CHUNKS = 3,      /* R < 1 or R > Nk, or chunk index out of range                   */
   RINGX_E_UNSUPPORTED = 4, /* dtype or head dim not supported (bf16: d in {64,128}; fp32: 1..128) */
   RINGX_E_ALIGN = 5,       /* a tensor pointer is not 16-byte aligned                        */

@@ -127,9 +127,12 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
       static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(dout + qh0 * Nq * D)));
   const float* nlb = static_cast<const float*>(uniform_ptr(nl + qh0 * Nq));
   const float* deltab = static_cast<const float*>(uniform_ptr(delta + qh0 * Nq));
-  const int nqt = (int)((Nq + C::kBQ - 1) / C::kBQ);
+  // query positions within a head are 32-bit (the library takes at most 2^31 queries per head),
+  // so that the tile bookkeeping below stays scalar instructions
+  const int nq = (int)Nq;
+  const int nqt = (nq + C::kBQ - 1) / C::kBQ;
   const int ntiles = grp * nqt;
-  const int tail = (int)(Nq - (nqt - 1) * C::kBQ);   // valid rows of a head's last tile
+  const int tail = nq - (nqt - 1) * C::kBQ;   // valid rows of a head's last tile
 
   // Per-lane offsets of the tile loads: load round u covers rows 16 u + (wave * 64 + lane) / 16
   // (d = 128) at a swizzled 16-byte chunk, so the offsets of round u are those of round 0 plus u
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     const char* qs = qb + ld_row * C::kRowBytes;
     const char* os = ob + ld_row * C::kRowBytes;
     const uint32_t dst = lbase + stage * C::kStage + wdst;
-    if (ld_r + C::kBQ <= Nq) {
+    if (ld_r + C::kBQ <= nq) {
 #pragma unroll
       for (int u = 0; u < C::kLoads; ++u) {
         load_lds16_s(qs + u * kRound, goff, dst + u * kRound);
@@ -158,7 +161,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     } else {
       // a head's last tile: rows past Nq are clamped to Nq - 1
       cold_path();
-      const int last = (int)(Nq - 1 - ld_r);
+      const int last = nq - 1 - ld_r;
 #pragma unroll
       for (int u = 0; u < C::kLoads; ++u) {
         const int row = row0 + u * (kRound / C::kRowBytes);
@@ -172,8 +175,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     }
     ld_r += C::kBQ;
     ld_row += C::kBQ;
-    if (ld_r >= Nq) {
-      ld_row += Nq - ld_r;   // next head
+    if (ld_r >= nq) {
+      ld_row += nq - ld_r;   // next head
       ld_r = 0;
     }
   };
@@ -461,8 +464,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
     }
     __syncthreads();
     nx_r += C::kBQ;
-    if (nx_r >= Nq) nx_r = 0;
-    if (it + 1 < ntiles && nx_r + C::kBQ > Nq) {
+    if (nx_r >= nq) nx_r = 0;
+    if (it + 1 < ntiles && nx_r + C::kBQ > nq) {
       cold_path();
       zero_tail((int)((it + 1) & 3));
       __syncthreads();

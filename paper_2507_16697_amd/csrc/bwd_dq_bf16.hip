@@ -103,19 +103,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
       static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(v + kvh * Nk * D)));
 
   // Tiles: chunk r covers keys [r Nk / R, (r+1) Nk / R), cut into 64-key tiles from its start.
-  // ld_*: the next tile to load; nx_*: the tile after the one being computed.
-  int64_t ld_start = 0, ld_hi = Nk / R;
-  int ld_r = 0;
-  int64_t nx_start = 0, nx_hi = Nk / R;
-  int nx_r = 0;
-  auto advance = [&](int64_t& start, int64_t& hi, int& r) {
-    start += C::kBK;
-    if (start >= hi) {
-      ++r;
-      start = hi;
-      hi = (int64_t)(r + 1) * Nk / R;
-    }
-  };
+  // ld_t: the next tile to load; nx_t: the tile after the one being computed (32-bit positions
+  // walked without divisions, so that the loop's bookkeeping stays scalar).
+  const uint32_t nk = (uint32_t)Nk;
+  ChunkWalk ld_w{nk, nk / (uint32_t)R, nk % (uint32_t)R, 0, (uint32_t)R};
+  ChunkWalk nx_w = ld_w;
+  KeyTile ld_t = ld_w.first();
+  KeyTile nx_t = nx_w.first();
   int ntiles = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t lo = (int64_t)r * Nk / R, hi = (int64_t)(r + 1) * Nk / R;
@@ -132,10 +126,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
       row0 * C::kRowBytes + (((wave * 64 + lane) % C::kChunks) ^ swz<D>(row0)) * 16;
   const uint32_t wdst = (uint32_t)__builtin_amdgcn_readfirstlane(wave * 1024);
   auto issue_next = [&](int stage) {
-    const char* ks = kb + ld_start * C::kRowBytes;
-    const char* vs = vb + ld_start * C::kRowBytes;
+    const char* ks = kb + (uint64_t)ld_t.start * C::kRowBytes;
+    const char* vs = vb + (uint64_t)ld_t.start * C::kRowBytes;
     const uint32_t dst = lbase + stage * C::kStage + wdst;
-    if (ld_start + C::kBK <= ld_hi) {
+    if (ld_t.start + C::kBK <= ld_t.hi) {
 #pragma unroll
       for (int u = 0; u < C::kLoads; ++u) {
         load_lds16_s(ks + u * kRound, goff, dst + u * kRound);
@@ -144,7 +138,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     } else {
       // the last tile of a chunk: rows past its end are clamped to the chunk's last key
       cold_path();
-      const int last = (int)(ld_hi - 1 - ld_start);
+      const int last = (int)(ld_t.hi - 1 - ld_t.start);
 #pragma unroll
       for (int u = 0; u < C::kLoads; ++u) {
         const int row = row0 + u * (kRound / C::kRowBytes);
@@ -153,7 +147,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
         load_lds16_s(vs, off, dst + C::kTile + u * kRound);
       }
     }
-    advance(ld_start, ld_hi, ld_r);
+    ld_t = ld_w.next<C::kBK>(ld_t);
   };
 
 #pragma unroll
@@ -223,7 +217,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
 
   // keys of the tile being computed (cur_valid) and of the next one (nx_valid) that lie inside
   // their chunk: 64 except in the last tile of a chunk
-  int cur_valid = (int)min<int64_t>(C::kBK, nx_hi - nx_start);
+  int cur_valid = (int)min<uint32_t>(C::kBK, nx_t.hi - nx_t.start);
   int nx_valid = C::kBK;
 
   wait_vmem<0>();
@@ -371,8 +365,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(
     if (it + 2 < ntiles) wait_vmem<C::kTileOps>();
     else wait_vmem<0>();
     __syncthreads();
-    advance(nx_start, nx_hi, nx_r);
-    if (it + 1 < ntiles) nx_valid = (int)min<int64_t>(C::kBK, nx_hi - nx_start);
+    nx_t = nx_w.next<C::kBK>(nx_t);
+    if (it + 1 < ntiles) nx_valid = (int)min<uint32_t>(C::kBK, nx_t.hi - nx_t.start);
     if (it + 3 < ntiles) issue_next((it + 3) & 3);
     __builtin_amdgcn_sched_barrier(0);
 

@@ -98,56 +98,30 @@ __device__ __forceinline__ void load_offsets(int (&goff)[FwdCfg<D>::kLoads],
 
 // Issue the direct loads of one K or V tile starting at key `start` into the LDS buffer at
 // `dst`; rows at or past `hi` (only in the last tile of a chunk) are clamped to hi - 1.
+// `wdst` is the loader wave's first 1 KiB slot (wave * 1024, an SGPR).
 template <int D>
 __device__ __forceinline__ void issue_tile(const char* __restrict__ base, uint32_t dst,
-                                           int64_t start, int64_t hi,
+                                           uint32_t start, uint32_t hi,
                                            const int (&goff)[FwdCfg<D>::kLoads],
-                                           const int (&grow)[FwdCfg<D>::kLoads], int wave) {
+                                           const int (&grow)[FwdCfg<D>::kLoads], int wave,
+                                           uint32_t wdst) {
   using C = FwdCfg<D>;
   if (wave >= C::kLoaders) return;
-  const char* src = base + start * C::kRowBytes;
+  const char* src = base + (uint64_t)start * C::kRowBytes;
   if (start + C::kBK <= hi) {
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u)
-      load_lds16_s(src, (uint32_t)goff[u],
-                   dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kLoaders + wave) * 1024));
+      load_lds16_s(src, (uint32_t)goff[u], dst + wdst + u * C::kLoaders * 1024);
   } else {
     cold_path();
     const int last = (int)(hi - 1 - start);
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
       const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
-      load_lds16_s(src, (uint32_t)off,
-                   dst + (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kLoaders + wave) * 1024));
+      load_lds16_s(src, (uint32_t)off, dst + wdst + u * C::kLoaders * 1024);
     }
   }
 }
-
-// The chunked key sequence, walked one tile at a time (chunk r = [floor(r Nk/R), floor((r+1) Nk/R))
-// without divisions: chunk r has Nk/R keys plus one when the running remainder wraps).
-struct KeyTile {
-  int64_t start, hi;   // first key of the tile, end of its chunk; start >= Nk: no tile
-};
-
-struct ChunkWalk {
-  int64_t Nk, q_sz, rem, racc;
-  int R;
-  __device__ KeyTile first() {
-    racc = rem;
-    const int64_t extra = racc >= R ? 1 : 0;
-    racc -= extra * R;
-    return {0, q_sz + extra};
-  }
-  template <int BK>
-  __device__ KeyTile next(const KeyTile& t) {
-    if (t.start + BK < t.hi) return {t.start + BK, t.hi};
-    if (t.hi >= Nk) return {Nk, Nk};
-    racc += rem;
-    const int64_t extra = racc >= R ? 1 : 0;
-    racc -= extra * R;
-    return {t.hi, t.hi + q_sz + extra};
-  }
-};
 
 template <int D, int MODE>
 __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
@@ -183,7 +157,9 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
   int goff[C::kLoads], grow[C::kLoads];
   load_offsets<D>(goff, grow, wave, lane);
 
-  ChunkWalk walk{Nk, Nk / R, Nk % R, 0, R};
+  const uint32_t nk = (uint32_t)Nk;
+  ChunkWalk walk{nk, nk / (uint32_t)R, nk % (uint32_t)R, 0, (uint32_t)R};
+  uint32_t wdst = (uint32_t)__builtin_amdgcn_readfirstlane(wave * 1024);
   KeyTile t0 = walk.first();
   KeyTile t1 = walk.next<C::kBK>(t0);
   KeyTile t2 = walk.next<C::kBK>(t1);
@@ -194,9 +170,10 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
   const uint32_t lv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_v;
 
   // K_0, V_0 and K_1 in flight while Q is loaded
-  issue_tile<D>(kb, lk, t0.start, t0.hi, goff, grow, wave);
-  issue_tile<D>(vb, lv, t0.start, t0.hi, goff, grow, wave);
-  if (t1.start < Nk) issue_tile<D>(kb, lk + C::kTileBytes, t1.start, t1.hi, goff, grow, wave);
+  issue_tile<D>(kb, lk, t0.start, t0.hi, goff, grow, wave, wdst);
+  issue_tile<D>(vb, lv, t0.start, t0.hi, goff, grow, wave, wdst);
+  if (t1.start < nk)
+    issue_tile<D>(kb, lk + C::kTileBytes, t1.start, t1.hi, goff, grow, wave, wdst);
 
   // Q fragments (B operand of S^T = K Q^T): query n of this wave, dims 16*ks + 8g .. +8.
   bf16x8 qf[C::kDSteps];
@@ -257,17 +234,20 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     // K_{j+1} and V_j landed (issued one iteration ago); every wave is done with K_j, V_{j-1}
     wait_vmem_all();
     __syncthreads();
-    if (t2.start < Nk)
-      issue_tile<D>(kb, lk + P * C::kTileBytes, t2.start, t2.hi, goff, grow, wave);
-    if (t1.start < Nk)
-      issue_tile<D>(vb, lv + (1 - P) * C::kTileBytes, t1.start, t1.hi, goff, grow, wave);
+    // wdst counts as redefined here, so that the load slots' addresses are formed at each use
+    // (scalar adds) instead of being held in registers across the loop
+    asm volatile("" : "+s"(wdst));
+    if (t2.start < nk)
+      issue_tile<D>(kb, lk + P * C::kTileBytes, t2.start, t2.hi, goff, grow, wave, wdst);
+    if (t1.start < nk)
+      issue_tile<D>(vb, lv + (1 - P) * C::kTileBytes, t1.start, t1.hi, goff, grow, wave, wdst);
     // The vector work of this half (exponentials, row sums) is the longer chain; it issues ahead
     // of the other wave's matrix products on the SIMD, which fill the gaps (priority drops again
     // for the P V half).
     __builtin_amdgcn_s_setprio(1);
 
     // last tile of a chunk: keys past the chunk end (clamped copies of its last key) add nothing
-    const int nvalid = (int)min<int64_t>(C::kBK, t0.hi - t0.start);
+    const int nvalid = (int)min<uint32_t>(C::kBK, t0.hi - t0.start);
     if (nvalid < C::kBK) {
       cold_path();
       const int thr = nvalid - 4 * g;   // key 4g + off is past the end iff off >= thr
@@ -442,7 +422,7 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
     t0 = t1;
     t1 = t2;
     t2 = walk.next<C::kBK>(t2);
-    return t0.start >= Nk;
+    return t0.start >= nk;
   };
 
   while (true) {

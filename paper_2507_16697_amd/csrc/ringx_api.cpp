@@ -19,6 +19,8 @@ namespace {
 constexpr int64_t kMaxElems = int64_t(1) << 40;   // per tensor; keeps every index product in int64
 constexpr int64_t kMaxRowsF32 = 65535;            // fp32 kernels put B*H on grid.y
 constexpr int64_t kMaxKeys = int64_t(1) << 31;    // keeps r * Nk (chunk bounds) inside int64
+// queries per head: the kernels keep query positions in 32 bits, with a tile of headroom
+constexpr int64_t kMaxQueries = (int64_t(1) << 31) - 128;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -42,7 +44,7 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 
 ringx_status check_dims(int64_t B, int64_t H, int64_t Nq, int64_t Nk, int64_t d, int64_t R,
                         float scale, ringx_dtype dtype) {
-  if (B < 1 || H < 1 || Nq < 1 || Nk < 1 || Nk > kMaxKeys) return RINGX_E_SHAPE;
+  if (B < 1 || H < 1 || Nq < 1 || Nk < 1 || Nk > kMaxKeys || Nq > kMaxQueries) return RINGX_E_SHAPE;
   if (!(std::isfinite(scale) && scale > 0.f)) return RINGX_E_SHAPE;
   if (dtype != RINGX_BF16 && dtype != RINGX_FP32) return RINGX_E_UNSUPPORTED;
   if (dtype == RINGX_BF16 && d != 64 && d != 128) return RINGX_E_UNSUPPORTED;

@@ -52,6 +52,34 @@ __device__ __forceinline__ float max_halves(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// The chunked key sequence walked one tile of BK keys at a time, without divisions: chunk r is
+// [floor(r Nk / R), floor((r + 1) Nk / R)), which holds Nk / R keys plus one whenever the running
+// sum of the remainders Nk mod R passes a multiple of R.  Key positions are 32-bit (the library
+// takes at most 2^31 keys per head), so that the walk and its tests stay scalar instructions.
+struct KeyTile {
+  uint32_t start, hi;   // first key of the tile, end of its chunk; start >= Nk: no tile
+};
+
+struct ChunkWalk {
+  uint32_t Nk, q_sz, rem, racc;   // Nk, Nk / R, Nk mod R, running remainder
+  uint32_t R;
+  __device__ KeyTile first() {
+    racc = rem;
+    const uint32_t extra = racc >= R ? 1u : 0u;
+    racc -= extra * R;
+    return {0, q_sz + extra};
+  }
+  template <int BK>
+  __device__ KeyTile next(const KeyTile& t) {
+    if (t.start + BK < t.hi) return {t.start + BK, t.hi};
+    if (t.hi >= Nk) return {Nk, Nk};
+    racc += rem;
+    const uint32_t extra = racc >= R ? 1u : 0u;
+    racc -= extra * R;
+    return {t.hi, t.hi + q_sz + extra};
+  }
+};
+
 // K/V head serving query head `bh` (of B*H): query heads come in consecutive groups of `grp` per
 // K/V head (grouped-query attention; grp = 1 is plain multi-head attention).
 __device__ __forceinline__ int64_t kv_head(int64_t bh, int H, int grp) {

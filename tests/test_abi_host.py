@@ -88,6 +88,7 @@ def test_forward_validation(fn):
     assert fn(q=0) == NULLPTR and fn(l=0) == NULLPTR and fn(o=0) == NULLPTR
     assert fn(B=0) == SHAPE and fn(H=-1) == SHAPE and fn(Nq=0) == SHAPE and fn(Nk=0) == SHAPE
     assert fn(Nk=(1 << 31) + 1, R=1) == SHAPE
+    assert fn(Nq=(1 << 31) - 127, B=1, H=1) == SHAPE               # queries per head above 2^31 - 128
     assert fn(scale=0.0) == SHAPE and fn(scale=float("nan")) == SHAPE and fn(scale=float("inf")) == SHAPE
     assert fn(scale=-1.0) == SHAPE
     assert fn(R=0) == CHUNKS and fn(R=301) == CHUNKS
