@@ -73,40 +73,36 @@ __device__ __forceinline__ int eoff(int row, int col) {
   return toff<RB>(row, col >> 3) + (col & 7) * 2;
 }
 
-// Rows row0 .. of a [N, D] bf16 matrix into a swizzled LDS tile at `dst` (rows clamped to
-// `last`), `per_wave` 1 KiB blocks per wave.
+// Rows of a [N, D] bf16 matrix from `src` (the tile's first row, the same for every lane) into a
+// swizzled LDS tile at `dst`, rows past `last` (relative to the first) clamped to it, `per_wave`
+// 1 KiB blocks per wave.  Scalar base plus 32-bit lane offsets: no per-lane 64-bit addresses.
 template <int D>
-__device__ __forceinline__ void issue_rows(const __bf16* __restrict__ src, uint32_t dst,
-                                           int64_t row0, int64_t last, int per_wave, int wave,
-                                           int lane, int nwaves) {
+__device__ __forceinline__ void issue_rows(const __bf16* __restrict__ src, uint32_t dst, int last,
+                                           int per_wave, int wave, int lane, int nwaves) {
   constexpr int kCh = D / 8;
   for (int u = 0; u < per_wave; ++u) {
     const int blk = u * nwaves + wave;
     const int slot = blk * 64 + lane;
     const int row = slot / kCh;
     const int c = (slot % kCh) ^ swz<2 * D>(row);
-    int64_t r = row0 + row;
-    r = r < last ? r : last;
-    load_lds16(src + r * D + c * 8, dst + (uint32_t)__builtin_amdgcn_readfirstlane(blk * 1024));
+    const int rr = row < last ? row : last;
+    load_lds16_s(src, (uint32_t)(rr * 2 * D + c * 16), dst + (uint32_t)(blk * 1024));
   }
 }
 
-// nl and D of queries row0 .. row0 + BQ - 1 (clamped to `last`) into LDS, 4 bytes per lane:
-// waves 0 and 1 load nl, waves 2 and 3 load D.
+// nl and D of the BQ queries from `nlb` / `deltab` (the tile's first row; rows past `last`
+// clamped to it) into LDS, 4 bytes per lane: waves 0 and 1 load nl, waves 2 and 3 load D.
 template <int BQ>
 __device__ __forceinline__ void issue_rowvals(const float* __restrict__ nlb,
                                               const float* __restrict__ deltab, uint32_t ldst,
-                                              uint32_t ddst, int64_t row0, int64_t last,
-                                              int wave, int lane) {
+                                              uint32_t ddst, int last, int wave, int lane) {
   static_assert(BQ <= 128, "two waves per array");
   const int part = wave & 1;
   if (wave < 4 && part * 64 < BQ) {
-    int64_t r = row0 + part * 64 + lane;
+    int r = part * 64 + lane;
     r = r < last ? r : last;
-    if (wave < 2)
-      load_lds4(nlb + r, ldst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
-    else
-      load_lds4(deltab + r, ddst + (uint32_t)__builtin_amdgcn_readfirstlane(part * 256));
+    if (wave < 2) load_lds4_s(nlb, (uint32_t)(4 * r), ldst + (uint32_t)(part * 256));
+    else load_lds4_s(deltab, (uint32_t)(4 * r), ddst + (uint32_t)(part * 256));
   }
 }
 
@@ -123,7 +119,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int wave = t >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int n = lane & 31;
   const int g = lane >> 5;
   const int kb = wave & 3;          // key block of this wave
@@ -151,18 +147,21 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   const float* nlb = nl + qh0 * Nq;
   const float* deltab = delta + qh0 * Nq;
 
-  const int64_t nqt = (Nq + C::kBQ - 1) / C::kBQ;
+  // query positions within a head are 32-bit (the library takes at most 2^31 queries per head),
+  // so that the tile bookkeeping stays scalar instructions
+  const int nq = (int)Nq;
+  const int nqt = (nq + C::kBQ - 1) / C::kBQ;
 
   // K and V tiles (kept for the whole sweep), then the first query tile
-  issue_rows<D>(kbp, lbase + C::kOffK, k0, hi - 1, C::kKTile / 1024 / C::kWaves, wave, lane,
+  issue_rows<D>(kbp + k0 * D, lbase + C::kOffK, (int)(hi - 1 - k0), C::kKTile / 1024 / C::kWaves,
+                wave, lane, C::kWaves);
+  issue_rows<D>(vbp + k0 * D, lbase + C::kOffV, (int)(hi - 1 - k0), C::kKTile / 1024 / C::kWaves,
+                wave, lane, C::kWaves);
+  issue_rows<D>(qb, lbase + C::kOffQ, nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
                 C::kWaves);
-  issue_rows<D>(vbp, lbase + C::kOffV, k0, hi - 1, C::kKTile / 1024 / C::kWaves, wave, lane,
+  issue_rows<D>(ob, lbase + C::kOffO, nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
                 C::kWaves);
-  issue_rows<D>(qb, lbase + C::kOffQ, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
-                C::kWaves);
-  issue_rows<D>(ob, lbase + C::kOffO, 0, Nq - 1, C::kQTile / 1024 / C::kWaves, wave, lane,
-                C::kWaves);
-  issue_rowvals<C::kBQ>(nlb, deltab, lbase + C::kOffL, lbase + C::kOffD, 0, Nq - 1, wave, lane);
+  issue_rowvals<C::kBQ>(nlb, deltab, lbase + C::kOffL, lbase + C::kOffD, nq - 1, wave, lane);
   const float* lds_l = reinterpret_cast<const float*>(lds + C::kOffL);
   const float* lds_d = reinterpret_cast<const float*>(lds + C::kOffD);
 
@@ -196,28 +195,29 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   wait_vmem_all();
   __syncthreads();
 
-  const int64_t ntiles = (int64_t)grp * nqt;
-  int64_t q0 = 0;     // first row of the current tile within its head
-  int64_t qn = 0;     // first row of the next tile, and the offset (in rows) of its head
-  int64_t hn = 0;
-  for (int64_t it = 0; it < ntiles; ++it) {
-    const int cur = (int)(it & 1);
+  const int ntiles = grp * nqt;
+  int q0 = 0;         // first row of the current tile within its head
+  int qn = 0;         // first row of the next tile
+  int64_t hn = 0;     // the offset (in rows) of the next tile's head
+  for (int it = 0; it < ntiles; ++it) {
+    const int cur = it & 1;
     // next query tile in flight: Q, dO rows and their nl, D straight into LDS
     qn = q0 + C::kBQ;
-    if (qn >= Nq) {
+    if (qn >= nq) {
       qn = 0;
       hn += Nq;
     }
     if (it + 1 < ntiles) {
-      issue_rows<D>(qb + hn * D, lbase + C::kOffQ + (cur ^ 1) * C::kQTile, qn, Nq - 1,
+      const int64_t row = hn + qn;
+      issue_rows<D>(qb + row * D, lbase + C::kOffQ + (cur ^ 1) * C::kQTile, nq - 1 - qn,
                     C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rows<D>(ob + hn * D, lbase + C::kOffO + (cur ^ 1) * C::kQTile, qn, Nq - 1,
+      issue_rows<D>(ob + row * D, lbase + C::kOffO + (cur ^ 1) * C::kQTile, nq - 1 - qn,
                     C::kQTile / 1024 / C::kWaves, wave, lane, C::kWaves);
-      issue_rowvals<C::kBQ>(nlb + hn, deltab + hn, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
-                            lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, qn, Nq - 1, wave, lane);
+      issue_rowvals<C::kBQ>(nlb + row, deltab + row, lbase + C::kOffL + (cur ^ 1) * C::kBQ * 4,
+                            lbase + C::kOffD + (cur ^ 1) * C::kBQ * 4, nq - 1 - qn, wave, lane);
     }
     // last query tile (rows past Nq are clamped copies) or a partial key tile
-    const bool masked = q0 + C::kBQ > Nq || nvalid < C::kBK;
+    const bool masked = q0 + C::kBQ > nq || nvalid < C::kBK;
     const char* qt = lds + C::kOffQ + cur * C::kQTile;
     const char* ot = lds + C::kOffO + cur * C::kQTile;
     const char* kt = lds + C::kOffK;
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
           const int qi = qh * C::kQW + 32 * b + 8 * (rr >> 2) + 4 * g + (rr & 3);
-          if (!key_ok || q0 + qi >= Nq) {
+          if (!key_ok || q0 + qi >= nq) {
             p[rr] = 0.f;
             dsv[rr] = 0.f;
           }

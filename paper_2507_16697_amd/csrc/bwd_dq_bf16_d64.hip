@@ -66,23 +66,22 @@ __device__ __forceinline__ void load_offsets(int (&goff)[DqCfg<D>::kLoads],
 }
 
 // Direct loads of one K/V tile starting at key `start`; rows at or past `hi` (only in the last
-// tile of a chunk) are clamped to hi - 1.
+// tile of a chunk) are clamped to hi - 1.  Scalar tile bases plus 32-bit lane offsets.
 template <int D>
 __device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
                                            const char* __restrict__ vb, uint32_t kdst,
-                                           uint32_t vdst, int64_t start, int64_t hi,
+                                           uint32_t vdst, uint32_t start, uint32_t hi,
                                            const int (&goff)[DqCfg<D>::kLoads],
                                            const int (&grow)[DqCfg<D>::kLoads], int wave) {
   using C = DqCfg<D>;
-  const char* kt = kb + start * C::kRowBytes;
-  const char* vt = vb + start * C::kRowBytes;
+  const char* kt = kb + (uint64_t)start * C::kRowBytes;
+  const char* vt = vb + (uint64_t)start * C::kRowBytes;
   if (start + C::kBK <= hi) {
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
-      const uint32_t wbase =
-          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
-      load_lds16(kt + goff[u], kdst + wbase);
-      load_lds16(vt + goff[u], vdst + wbase);
+      const uint32_t wbase = (uint32_t)((u * C::kWaves + wave) * 1024);
+      load_lds16_s(kt, (uint32_t)goff[u], kdst + wbase);
+      load_lds16_s(vt, (uint32_t)goff[u], vdst + wbase);
     }
   } else {
     cold_path();
@@ -90,10 +89,9 @@ __device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
       const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
-      const uint32_t wbase =
-          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
-      load_lds16(kt + off, kdst + wbase);
-      load_lds16(vt + off, vdst + wbase);
+      const uint32_t wbase = (uint32_t)((u * C::kWaves + wave) * 1024);
+      load_lds16_s(kt, (uint32_t)off, kdst + wbase);
+      load_lds16_s(vt, (uint32_t)off, vdst + wbase);
     }
   }
 }
@@ -110,7 +108,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
 
   const int t = threadIdx.x;
   const int lane = t & 63;
-  const int wave = t >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int n = lane & 31;
   const int g = lane >> 5;
 
@@ -121,23 +119,21 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
   if (bh >= BH) return;
 
   const int64_t kvh = kv_head(bh, H, grp);
-  const char* kb = reinterpret_cast<const char*>(k + kvh * Nk * D);
-  const char* vb = reinterpret_cast<const char*>(v + kvh * Nk * D);
+  const char* kb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(k + kvh * Nk * D)));
+  const char* vb =
+      static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(v + kvh * Nk * D)));
   int goff[C::kLoads], grow[C::kLoads];
   load_offsets<D>(goff, grow, wave, lane);
 
-  // chunk bookkeeping without divisions (see the forward kernel)
-  const int64_t q_sz = Nk / R;
-  const int64_t rem = Nk % R;
-  int64_t racc = rem;
-  int64_t hi = q_sz;
-  if (racc >= R) { racc -= R; hi += 1; }
-  int r = 0;
-  int64_t start = 0;
+  // the chunked key sequence, one tile at a time (32-bit positions, no divisions)
+  const uint32_t nk = (uint32_t)Nk;
+  ChunkWalk walk{nk, nk / (uint32_t)R, nk % (uint32_t)R, 0, (uint32_t)R};
+  KeyTile ct = walk.first();
 
   const uint32_t lk = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_k;
   const uint32_t lv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_v;
-  issue_tile<D>(kb, vb, lk, lv, start, hi, goff, grow, wave);
+  issue_tile<D>(kb, vb, lk, lv, ct.start, ct.hi, goff, grow, wave);
 
   // this lane's query: Q and dO fragments (B operands), -lse*log2e and D
   int64_t qi = q0 + n;
@@ -187,26 +183,15 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
   __syncthreads();
 
   while (true) {
-    int64_t nstart = start + C::kBK;
-    int64_t nhi = hi;
-    bool has_next = true;
-    if (nstart >= hi) {
-      if (r + 1 < R) {
-        nstart = hi;
-        racc += rem;
-        nhi = hi + q_sz;
-        if (racc >= R) { racc -= R; nhi += 1; }
-      } else {
-        has_next = false;
-      }
-    }
+    const KeyTile nt = walk.next<C::kBK>(ct);
+    const bool has_next = nt.start < nk;
     if (has_next)
       issue_tile<D>(kb, vb, lk + (cur ^ 1) * C::kTileBytes, lv + (cur ^ 1) * C::kTileBytes,
-                    nstart, nhi, goff, grow, wave);
+                    nt.start, nt.hi, goff, grow, wave);
 
     const char* kbuf = lds_k + cur * C::kTileBytes;
     const char* vbuf = lds_v + cur * C::kTileBytes;
-    const int nvalid = (int)min<int64_t>(C::kBK, hi - start);
+    const int nvalid = (int)min<uint32_t>(C::kBK, ct.hi - ct.start);
 
     f32x16 sacc[C::kKTiles], pacc[C::kKTiles];
 #pragma unroll
@@ -272,13 +257,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
 
-    if (start + C::kBK >= hi) ++r;
     if (!has_next) break;
     wait_vmem_all();
     __syncthreads();
     cur ^= 1;
-    start = nstart;
-    hi = nhi;
+    ct = nt;
   }
 
   if (q_ok) {
