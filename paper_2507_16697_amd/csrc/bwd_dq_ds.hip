@@ -96,22 +96,15 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_ds_kernel(
     const int64_t lo = (int64_t)r * Nk / R, hi = (int64_t)(r + 1) * Nk / R;
     ntiles += (int)((hi - lo + C::kBK - 1) / C::kBK);
   }
-  // the next tile to load: key range start, chunk end, chunk, tile within the chunk
-  int64_t ld_start = 0, ld_hi = Nk / R;
-  int ld_r = 0, ld_t = 0;
-  // the tile being computed
-  int64_t cu_start = 0, cu_hi = Nk / R;
-  int cu_r = 0, cu_t = 0;
-  auto advance = [&](int64_t& start, int64_t& hi, int& r, int& tt) {
-    start += C::kBK;
-    ++tt;
-    if (start >= hi) {
-      ++r;
-      tt = 0;
-      start = hi;
-      hi = (int64_t)(r + 1) * Nk / R;
-    }
-  };
+  // the next tile to load (ld_k, its chunk ld_r and key-block pair ld_pair = ld_r 2 tpc + its
+  // tile within the chunk) and the tile being computed (cu_k): 32-bit positions walked without
+  // divisions, so that the loop's bookkeeping stays scalar
+  const uint32_t nk = (uint32_t)Nk;
+  ChunkWalk ld_w{nk, nk / (uint32_t)R, nk % (uint32_t)R, 0, (uint32_t)R};
+  ChunkWalk cu_w = ld_w;
+  KeyTile ld_k = ld_w.first();
+  KeyTile cu_k = cu_w.first();
+  int ld_r = 0, ld_pair = 0;
 
   // K loads: round u covers rows 16 u + (wave * 64 + lane) / 16 at a swizzled chunk
   constexpr uint32_t kRound = C::kWaves * 64 * 16;
@@ -125,16 +118,16 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_ds_kernel(
   static_assert(C::kDsLoads == 4 && kRound == 2 * kDsUnitBytes, "two rounds per key block");
   const uint32_t wdst = (uint32_t)__builtin_amdgcn_readfirstlane(wave * 1024);
   auto issue_next = [&](int stage) {
-    const char* kt = kbase + ld_start * C::kRowBytes;
-    // key blocks 2 p and 2 p + 1 of the pair p = ld_r 2 tpc + ld_t; round u takes half u % 2 of
-    // block u / 2's 8 KiB
-    const char* dt = dsbase + ((int64_t)ld_r * 2 * tpc + ld_t) * 2 * kbstride;
+    const char* kt = kbase + (uint64_t)ld_k.start * C::kRowBytes;
+    // key blocks 2 p and 2 p + 1 of the pair p = ld_pair; round u takes half u % 2 of block
+    // u / 2's 8 KiB
+    const char* dt = dsbase + (int64_t)ld_pair * 2 * kbstride;
     const uint32_t dst = lbase + stage * C::kStage + wdst;
 #pragma unroll
     for (int u = 0; u < C::kDsLoads; ++u)
       load_lds16_s(dt + (u >> 1) * kbstride + (u & 1) * kRound + wave * 1024, dsoff,
                    dst + u * kRound);
-    if (ld_start + C::kBK <= ld_hi) {
+    if (ld_k.start + C::kBK <= ld_k.hi) {
 #pragma unroll
       for (int u = 0; u < C::kLoads; ++u)
         load_lds16_s(kt + u * kRound, goff, dst + C::kDsTile + u * kRound);
@@ -142,7 +135,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_ds_kernel(
       // the last tile of a chunk: rows past its end are clamped to the chunk's last key (and
       // zeroed once landed)
       cold_path();
-      const int last = (int)(ld_hi - 1 - ld_start);
+      const int last = (int)(ld_k.hi - 1 - ld_k.start);
 #pragma unroll
       for (int u = 0; u < C::kLoads; ++u) {
         const int row = row0 + u * (kRound / C::kRowBytes);
@@ -150,7 +143,13 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_ds_kernel(
         load_lds16_s(kt, off, dst + C::kDsTile + u * kRound);
       }
     }
-    advance(ld_start, ld_hi, ld_r, ld_t);
+    if (ld_k.start + C::kBK < ld_k.hi) {
+      ++ld_pair;
+    } else {
+      ++ld_r;
+      ld_pair = ld_r * 2 * tpc;
+    }
+    ld_k = ld_w.next<C::kBK>(ld_k);
   };
 
 #pragma unroll
@@ -198,7 +197,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_ds_kernel(
     static_assert(C::kStages == 2, "nothing is in flight beyond the next tile");
     wait_vmem<0>();
     __syncthreads();
-    const int valid = (int)min<int64_t>(C::kBK, cu_hi - cu_start);
+    const int valid = (int)min<uint32_t>(C::kBK, cu_k.hi - cu_k.start);
     if (valid < C::kBK) {
       // rows valid .. 63 of the K tile belong to no key
       cold_path();
@@ -209,7 +208,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_ds_kernel(
       __syncthreads();
     }
     if (it + C::kStages - 1 < ntiles) issue_next((it + C::kStages - 1) % C::kStages);
-    advance(cu_start, cu_hi, cu_r, cu_t);
+    cu_k = cu_w.next<C::kBK>(cu_k);
 
     const char* dsl = lds + st;
     const char* kl = lds + st + C::kDsTile;
