@@ -127,8 +127,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(
       static_cast<const char*>(uniform_ptr(reinterpret_cast<const char*>(dout + qh0 * Nq * D)));
   const float* nlb = static_cast<const float*>(uniform_ptr(nl + qh0 * Nq));
   const float* deltab = static_cast<const float*>(uniform_ptr(delta + qh0 * Nq));
-  // query positions within a head are 32-bit (the library takes at most 2^31 - 128 queries per head),
-  // so that the tile bookkeeping below stays scalar instructions
+  // query positions within a head are 32-bit (the library takes at most 2^31 - 128 queries
+  // per head), so that the tile bookkeeping below stays scalar instructions
   const int nq = (int)Nq;
   const int nqt = (nq + C::kBQ - 1) / C::kBQ;
   const int ntiles = grp * nqt;

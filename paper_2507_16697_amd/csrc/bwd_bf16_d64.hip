@@ -147,8 +147,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
   const float* nlb = nl + qh0 * Nq;
   const float* deltab = delta + qh0 * Nq;
 
-  // query positions within a head are 32-bit (the library takes at most 2^31 - 128 queries per head),
-  // so that the tile bookkeeping stays scalar instructions
+  // query positions within a head are 32-bit (the library takes at most 2^31 - 128 queries
+  // per head), so that the tile bookkeeping stays scalar instructions
   const int nq = (int)Nq;
   const int nqt = (nq + C::kBQ - 1) / C::kBQ;
 
