@@ -286,9 +286,10 @@ __global__ __launch_bounds__(512, 1) void fwd_bf16_kernel(
       }
     // at d = 128, four vector-ALU instructions (and, with them, two exponentials) beside each of
     // the 16 S products spread the tile's exponentials evenly over them (seven per product
-    // front-loaded them onto the first nine and ran 1.5% slower); d = 64 has half as many
-    // products for the same vector work and takes seven per product (0.4% faster than four)
-    constexpr int kValuPerProduct = D == 128 ? 4 : 7;
+    // front-loaded them onto the first nine and ran 1.5% slower; three and five were 0.3% and
+    // 1.1% slower); d = 64 has half as many products for the same vector work and takes eight
+    // per product (2-4% faster than seven, nine or ten)
+    constexpr int kValuPerProduct = D == 128 ? 4 : 8;
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
     for (int i = 0; i < C::kDSteps * C::kKTiles; ++i) {
