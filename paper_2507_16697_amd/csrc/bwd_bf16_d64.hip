@@ -86,7 +86,8 @@ __device__ __forceinline__ void issue_rows(const __bf16* __restrict__ src, uint3
     const int row = slot / kCh;
     const int c = (slot % kCh) ^ swz<2 * D>(row);
     const int rr = row < last ? row : last;
-    load_lds16_s(src, (uint32_t)(rr * 2 * D + c * 16), dst + (uint32_t)(blk * 1024));
+    load_lds16_s(src, (uint32_t)(rr * 2 * D + c * 16),
+                 dst + (uint32_t)__builtin_amdgcn_readfirstlane(blk * 1024));
   }
 }
 
@@ -101,8 +102,9 @@ __device__ __forceinline__ void issue_rowvals(const float* __restrict__ nlb,
   if (wave < 4 && part * 64 < BQ) {
     int r = part * 64 + lane;
     r = r < last ? r : last;
-    if (wave < 2) load_lds4_s(nlb, (uint32_t)(4 * r), ldst + (uint32_t)(part * 256));
-    else load_lds4_s(deltab, (uint32_t)(4 * r), ddst + (uint32_t)(part * 256));
+    const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane(part * 256);
+    if (wave < 2) load_lds4_s(nlb, (uint32_t)(4 * r), ldst + slot);
+    else load_lds4_s(deltab, (uint32_t)(4 * r), ddst + slot);
   }
 }
 

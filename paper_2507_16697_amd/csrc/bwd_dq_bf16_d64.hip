@@ -79,7 +79,8 @@ __device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
   if (start + C::kBK <= hi) {
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
-      const uint32_t wbase = (uint32_t)((u * C::kWaves + wave) * 1024);
+      const uint32_t wbase =
+          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
       load_lds16_s(kt, (uint32_t)goff[u], kdst + wbase);
       load_lds16_s(vt, (uint32_t)goff[u], vdst + wbase);
     }
@@ -89,7 +90,8 @@ __device__ __forceinline__ void issue_tile(const char* __restrict__ kb,
 #pragma unroll
     for (int u = 0; u < C::kLoads; ++u) {
       const int off = grow[u] <= last ? goff[u] : goff[u] - (grow[u] - last) * C::kRowBytes;
-      const uint32_t wbase = (uint32_t)((u * C::kWaves + wave) * 1024);
+      const uint32_t wbase =
+          (uint32_t)__builtin_amdgcn_readfirstlane((u * C::kWaves + wave) * 1024);
       load_lds16_s(kt, (uint32_t)off, kdst + wbase);
       load_lds16_s(vt, (uint32_t)off, vdst + wbase);
     }
