@@ -11,12 +11,14 @@
 // shares the K/V head when G > 1 query heads share one (grouped-query attention).  Wave w owns keys
 // 32*(w%4) .. +31 of the tile and query half w/4 of every query tile, and keeps fp32 dK^T, dV^T
 // accumulators for its keys in registers.  Per query tile:
-//   S   = Q K^T        A = Q rows (LDS),  B = K rows (LDS)              -> lane = key
-//   dP  = dO V^T       A = dO rows (LDS), B = V rows (LDS)
-//   P   = exp2(S*scale*log2e + nl_i),  dS = P (dP - D_i)                (fp32; nl_i = -lse_i*log2e
-//                                                                      from the preprocess)
-//   dV^T += dO^T P     A = dO^T by transposed LDS reads, B = P from registers
-//   dK^T += Q^T dS     A = Q^T by transposed LDS reads,  B = dS from registers
+//   S    = Q K^T        A = Q rows (LDS),  B = K rows (LDS)             -> lane = key
+//   D-dP = D + dO (-V)^T A = dO rows (LDS), B = -V rows (LDS), accumulators start at D
+//   P    = exp2(S*scale*log2e + nl_i),  -dS = P (D - dP)                (fp32; nl_i = -lse_i*log2e
+//                                                                       from the preprocess)
+//   dV^T += dO^T P       A = dO^T by transposed LDS reads, B = P from registers
+//   -dK^T += Q^T (-dS)   A = Q^T by transposed LDS reads,  B = -dS from registers
+// (the V tile is negated in LDS once it lands; negating V and dK is exact, and lets the matrix
+// cores subtract D)
 // Q, dO, nl and D of the next query tile arrive by direct global->LDS loads while the current
 // one is processed (double buffered, one barrier per tile).  K and V tiles are row-major in LDS
 // with XOR-swizzled 16-byte chunks.  The two waves sharing a key block add their dK/dV through
@@ -196,6 +198,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 
   wait_vmem_all();
   __syncthreads();
+  // -V, once for the whole sweep
+  for (int i = t; i < C::kKTile / 16; i += C::kThreads) {
+    u32x4* x = reinterpret_cast<u32x4*>(lds + C::kOffV) + i;
+    *x ^= (u32x4)0x80008000u;
+  }
+  __syncthreads();
 
   const int ntiles = grp * nqt;
   int q0 = 0;         // first row of the current tile within its head
@@ -227,12 +235,20 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     const float* cl = lds_l + cur * C::kBQ;
     const float* cd = lds_d + cur * C::kBQ;
 
-    // S = Q K^T, dP = dO V^T for this wave's 32 keys and kQW queries
+    // S = Q K^T and D - dP = D + dO (-V)^T for this wave's 32 keys and kQW queries; the dP
+    // accumulators start from D in accumulator order (element 4 rq + x is query 8 rq + 4 g + x)
     f32x16 sacc[C::kQB], pacc[C::kQB];
 #pragma unroll
     for (int b = 0; b < C::kQB; ++b) {
       sacc[b] = f32x16{};
-      pacc[b] = f32x16{};
+      const float* db = cd + qh * C::kQW + 32 * b + 4 * g;
+      const f32x4 d0 = *reinterpret_cast<const f32x4*>(db);
+      const f32x4 d1 = *reinterpret_cast<const f32x4*>(db + 8);
+      const f32x4 d2 = *reinterpret_cast<const f32x4*>(db + 16);
+      const f32x4 d3 = *reinterpret_cast<const f32x4*>(db + 24);
+      pacc[b] = __builtin_shufflevector(__builtin_shufflevector(d0, d1, 0, 1, 2, 3, 4, 5, 6, 7),
+                                        __builtin_shufflevector(d2, d3, 0, 1, 2, 3, 4, 5, 6, 7),
+                                        0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12, 13, 14, 15);
     }
 #pragma unroll
     for (int s = 0; s < C::kDSteps; ++s) {
@@ -259,12 +275,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
       for (int rq = 0; rq < 4; ++rq) {
         const int qi = qh * C::kQW + 32 * b + 8 * rq + 4 * g;   // 4 consecutive queries
         const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + qi);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(cd + qi);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float pe = fast_exp2(__builtin_fmaf(sacc[b][4 * rq + e], c2, nl4[e]));
           p[4 * rq + e] = pe;
-          dsv[4 * rq + e] = pe * (pacc[b][4 * rq + e] - d4[e]);
+          dsv[4 * rq + e] = pe * pacc[b][4 * rq + e];   // -dS
         }
       }
       if (masked) {
@@ -341,7 +356,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
         for (int rr = 0; rr < 16; ++rr) acc[c][rr] += xch[((kb * C::kCT + c) * 16 + rr) * 64 + lane];
       if (key_ok) {
         float* dst = which == 0 ? dkr : dvr;
-        const float f = which == 0 ? scale : 1.0f;
+        const float f = which == 0 ? -scale : 1.0f;   // the dK^T accumulators hold sums of -dS
 #pragma unroll
         for (int c = 0; c < C::kCT; ++c)
 #pragma unroll
