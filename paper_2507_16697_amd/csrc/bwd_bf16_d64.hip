@@ -27,6 +27,7 @@
 #include "ringx_device.h"
 #include "ringx_kernels.h"
 
+
 namespace ringx {
 namespace {
 
@@ -45,14 +46,17 @@ struct DkvCfg {
   static constexpr int kCT = D / 32;
   static constexpr int kQTile = kBQ * kRowBytes;   // bytes of one Q or dO tile (16 KiB)
   static constexpr int kKTile = kBK * kRowBytes;   // bytes of the K or V tile
-  // LDS carve-up (bytes)
-  static constexpr int kOffK = 0;
-  static constexpr int kOffV = kOffK + kKTile;
-  static constexpr int kOffQ = kOffV + kKTile;          // 2 buffers
+  // LDS carve-up (bytes): the Q and dO buffers, read at every product, first, so that their
+  // offsets fit the 16-bit immediate of the LDS reads; K, V, nl and D are read from registers
+  // holding their bases
+  static constexpr int kOffQ = 0;                       // 2 buffers
   static constexpr int kOffO = kOffQ + 2 * kQTile;      // 2 buffers
-  static constexpr int kOffL = kOffO + 2 * kQTile;      // 2 x kBQ floats: nl
+  static constexpr int kOffK = kOffO + 2 * kQTile;
+  static constexpr int kOffV = kOffK + kKTile;
+  static constexpr int kOffL = kOffV + kKTile;          // 2 x kBQ floats: nl
   static constexpr int kOffD = kOffL + 2 * kBQ * 4;     // 2 x kBQ floats: D
   static constexpr int kLds = kOffD + 2 * kBQ * 4;
+  static_assert(kOffK <= 65536, "Q / dO buffers within the LDS immediate offset");
   static_assert(kQB * 32 * 2 == kBQ, "two query halves");
   static_assert(4 * kQTile >= kWaves / 2 * kCT * 16 * 64 * 4, "dK/dV exchange fits");
 };
@@ -186,6 +190,28 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 #pragma unroll
     for (int ct = 0; ct < C::kCT; ++ct)
       qtoff[h][ct] = eoff<2 * D>(4 * g + 8 * h + trr, 32 * ct + trc);
+  // the same offsets with this wave's key block (K/V rows) and query half (Q/dO rows, nl and D)
+  // folded in, as opaque registers: each read then adds only immediates (buffer, block, step)
+  int kvo[C::kDSteps], qo[C::kDSteps], tqo[2][C::kCT];
+#pragma unroll
+  for (int s = 0; s < C::kDSteps; ++s) {
+    kvo[s] = C::kOffK + aoff[s] + 32 * kb * C::kRowBytes;
+    qo[s] = aoff[s] + qh * C::kQW * C::kRowBytes;
+    asm volatile("" : "+v"(kvo[s]), "+v"(qo[s]));
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int ct = 0; ct < C::kCT; ++ct) {
+      tqo[h][ct] = qtoff[h][ct] + qh * C::kQW * C::kRowBytes;
+      asm volatile("" : "+v"(tqo[h][ct]));
+    }
+  int so = C::kOffL + 4 * (qh * C::kQW + 4 * g);   // this lane's first query in the nl array
+  asm volatile("" : "+v"(so));
+  static_assert(C::kOffQ % (2 * C::kQTile) == 0 && C::kQTile >= C::kQW * 2 * C::kRowBytes,
+                "Q / dO lane offsets below kQTile: xor with kQTile switches buffers");
+  static_assert(C::kOffL % (4 * C::kBQ * 4) == 0 && 4 * (C::kQW + 4) <= C::kBQ * 4,
+                "nl / D lane offsets below kBQ floats: xor with kBQ * 4 switches buffers");
 
   const bool key_ok = 32 * kb + n < nvalid;
 
@@ -228,12 +254,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     }
     // last query tile (rows past Nq are clamped copies) or a partial key tile
     const bool masked = q0 + C::kBQ > nq || nvalid < C::kBK;
-    const char* qt = lds + C::kOffQ + cur * C::kQTile;
-    const char* ot = lds + C::kOffO + cur * C::kQTile;
-    const char* kt = lds + C::kOffK;
-    const char* vt = lds + C::kOffV;
-    const float* cl = lds_l + cur * C::kBQ;
-    const float* cd = lds_d + cur * C::kBQ;
+    // qo, tqo and so point into buffer `cur` (toggled at the end of every tile)
+    const char* qt = lds + C::kOffQ;
+    const char* ot = lds + C::kOffO;
+    const char* kt = lds;                        // kvo[s] holds the K tile's base
+    const char* vt = lds + (C::kOffV - C::kOffK);
+    const char* cl = lds + so;                   // so holds the nl array's base
+    const char* cd = lds + so + (C::kOffD - C::kOffL);
 
     // S = Q K^T and D - dP = D + dO (-V)^T for this wave's 32 keys and kQW queries; the dP
     // accumulators start from D in accumulator order (element 4 rq + x is query 8 rq + 4 g + x)
@@ -241,7 +268,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
 #pragma unroll
     for (int b = 0; b < C::kQB; ++b) {
       sacc[b] = f32x16{};
-      const float* db = cd + qh * C::kQW + 32 * b + 4 * g;
+      const float* db = reinterpret_cast<const float*>(cd) + 32 * b;
       const f32x4 d0 = *reinterpret_cast<const f32x4*>(db);
       const f32x4 d1 = *reinterpret_cast<const f32x4*>(db + 8);
       const f32x4 d2 = *reinterpret_cast<const f32x4*>(db + 16);
@@ -252,13 +279,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     }
 #pragma unroll
     for (int s = 0; s < C::kDSteps; ++s) {
-      const bf16x8 bk = *reinterpret_cast<const bf16x8*>(kt + (32 * kb) * C::kRowBytes + aoff[s]);
-      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(vt + (32 * kb) * C::kRowBytes + aoff[s]);
+      const bf16x8 bk = *reinterpret_cast<const bf16x8*>(kt + kvo[s]);
+      const bf16x8 bv = *reinterpret_cast<const bf16x8*>(vt + kvo[s]);
 #pragma unroll
       for (int b = 0; b < C::kQB; ++b) {
-        const int rowb = (qh * C::kQW + 32 * b) * C::kRowBytes;
-        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(qt + rowb + aoff[s]);
-        const bf16x8 ao = *reinterpret_cast<const bf16x8*>(ot + rowb + aoff[s]);
+        const int rowb = 32 * b * C::kRowBytes;
+        const bf16x8 aq = *reinterpret_cast<const bf16x8*>(qt + rowb + qo[s]);
+        const bf16x8 ao = *reinterpret_cast<const bf16x8*>(ot + rowb + qo[s]);
         sacc[b] = mfma32(aq, bk, sacc[b]);
         pacc[b] = mfma32(ao, bv, pacc[b]);
       }
@@ -273,8 +300,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
       float p[16], dsv[16];
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
-        const int qi = qh * C::kQW + 32 * b + 8 * rq + 4 * g;   // 4 consecutive queries
-        const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + qi);
+        // nl of 4 consecutive queries qh kQW + 32 b + 8 rq + 4 g ..
+        const f32x4 nl4 = *reinterpret_cast<const f32x4*>(cl + 4 * (32 * b + 8 * rq));
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float pe = fast_exp2(__builtin_fmaf(sacc[b][4 * rq + e], c2, nl4[e]));
@@ -310,13 +337,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     // dV^T += dO^T P, dK^T += Q^T dS
 #pragma unroll
     for (int ks = 0; ks < 2 * C::kQB; ++ks) {
-      const int rowb = (qh * C::kQW + 16 * ks) * C::kRowBytes;
+      const int rowb = 16 * ks * C::kRowBytes;
 #pragma unroll
       for (int c = 0; c < C::kCT; ++c) {
-        const bf16x4 o0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + qtoff[0][c]));
-        const bf16x4 o1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + qtoff[1][c]));
-        const bf16x4 q0v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + qtoff[0][c]));
-        const bf16x4 q1v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + qtoff[1][c]));
+        const bf16x4 o0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + tqo[0][c]));
+        const bf16x4 o1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(ot + rowb + tqo[1][c]));
+        const bf16x4 q0v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + tqo[0][c]));
+        const bf16x4 q1v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(qt + rowb + tqo[1][c]));
         dvt[c] = mfma32(__builtin_shufflevector(o0, o1, 0, 1, 2, 3, 4, 5, 6, 7), pf[ks], dvt[c]);
         dkt[c] = mfma32(__builtin_shufflevector(q0v, q1v, 0, 1, 2, 3, 4, 5, 6, 7), sf[ks], dkt[c]);
       }
@@ -332,6 +359,16 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(
     wait_vmem_all();
     __syncthreads();
     q0 = qn;
+    // the read offsets move to the other buffer: its Q/dO tiles lie kQTile further (or back),
+    // its nl / D kBQ floats; the lane parts of the offsets stay below either step, so an exclusive
+    // or with the step switches buffers
+#pragma unroll
+    for (int s2 = 0; s2 < C::kDSteps; ++s2) qo[s2] ^= C::kQTile;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int ct = 0; ct < C::kCT; ++ct) tqo[h][ct] ^= C::kQTile;
+    so ^= C::kBQ * 4;
   }
 
   // the two query halves of a key block add their dK^T / dV^T through LDS
