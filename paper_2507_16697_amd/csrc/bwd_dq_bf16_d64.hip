@@ -175,6 +175,16 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
         toff[h][ct] = tile_off<D>(row, col >> 3) + (col & 7) * 2;
       }
   }
+  // The offsets address buffer `cur` of the K and V rings: an exclusive or with kTileBytes at the
+  // end of every tile switches them to the other buffer (their lane parts stay below it), so each
+  // read is one register plus an immediate.  Opaque, so that the compiler keeps them so.
+  static_assert(32 * C::kRowBytes <= C::kTileBytes, "lane offsets below one tile");
+#pragma unroll
+  for (int s = 0; s < C::kDSteps; ++s) asm volatile("" : "+v"(koff[s]));
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int c = 0; c < C::kCT; ++c) asm volatile("" : "+v"(toff[h][c]));
 
   f32x16 dqacc[C::kCT];
 #pragma unroll
@@ -191,8 +201,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
       issue_tile<D>(kb, vb, lk + (cur ^ 1) * C::kTileBytes, lv + (cur ^ 1) * C::kTileBytes,
                     nt.start, nt.hi, goff, grow, wave);
 
-    const char* kbuf = lds_k + cur * C::kTileBytes;
-    const char* vbuf = lds_v + cur * C::kTileBytes;
+    const char* kbuf = lds_k;   // koff and toff hold the buffer
+    const char* vbuf = lds_v;
     const int nvalid = (int)min<uint32_t>(C::kBK, ct.hi - ct.start);
 
     f32x16 sacc[C::kKTiles], pacc[C::kKTiles];
@@ -264,6 +274,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
     __syncthreads();
     cur ^= 1;
     ct = nt;
+#pragma unroll
+    for (int s = 0; s < C::kDSteps; ++s) koff[s] ^= C::kTileBytes;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int c = 0; c < C::kCT; ++c) toff[h][c] ^= C::kTileBytes;
   }
 
   if (q_ok) {
