@@ -367,6 +367,8 @@ PROFILE_DS = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ri
               "--no-merge --no-tokenizer --no-shapes --no-sclk")
 BUSY_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES SQ_VALU_MFMA_COEXEC_CYCLES SQ_BUSY_CYCLES "
                  "SQ_LDS_IDX_ACTIVE SQ_LDS_BANK_CONFLICT SQ_INSTS_LDS GRBM_GUI_ACTIVE")
+# L2 (TCC) hits and misses of the step's kernels (one counter pass; two of the four TCC counters)
+L2_COUNTERS = "TCC_HIT_sum TCC_MISS_sum"
 # instruction mix and wave states of every matrix kernel of the step and the other shapes (two
 # counter passes: at most 8 SQ counters per run)
 PROFILE_MIX = ("python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --no-ring --no-gqa "
@@ -604,6 +606,7 @@ def summarize_profiles(root, workload):
     with open(os.path.join(prof, f"mfma_busy_{workload}.md"), "w") as f:
         f.write("\n".join(md) + "\n")
     _summarize_stored_ds(root, workload, w, shape, prof, cmd, ff, wf)
+    _summarize_l2(root, workload, shape, prof, cmd, per_call)
     _summarize_instruction_mix(root, workload, prof, cmd)
     # the bench line of a plain `python bench.py` run beside the profiles, if there is one
     full = os.path.join(root, "bench.json")
@@ -616,6 +619,44 @@ def summarize_profiles(root, workload):
             json.dump(bench_line, f, indent=1)
             f.write("\n")
     print(f"wrote summaries of {root} under profiles/")
+
+
+def _summarize_l2(root, workload, shape, prof, cmd, per_call):
+    """L2 hit rate of the first call of each kernel of the step, from the TCC counter pass (when
+    it is there).  TCC requests are counted per cache line, whatever the request size."""
+    path = os.path.join(root, "pmc_l2", "pmc_counter_collection.csv")
+    if not os.path.exists(path):
+        return
+    disp = {}
+    for r in _read_csv(path):
+        e = disp.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
+        e[r["Counter_Name"]] = e.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    first = {}
+    for did in sorted(disp):
+        e = disp[did]
+        k = _profile_kernel(e["name"])
+        if not k:
+            continue
+        agg = first.setdefault(k[0], {"n": 0, "hit": 0.0, "miss": 0.0})
+        if agg["n"] >= per_call.get(k[0], 1):
+            continue
+        agg["n"] += 1
+        agg["hit"] += e.get("TCC_HIT_sum", 0.0)
+        agg["miss"] += e.get("TCC_MISS_sum", 0.0)
+    md = [f"# L2 hit rate: {workload} ({shape})", "",
+          "Command (run from the repository root on one MI355X, one counter pass):", "",
+          "    " + cmd("pmc_l2", "pmc", "--pmc " + L2_COUNTERS) + PROFILE_STEP, "",
+          "TCC_HIT_sum and TCC_MISS_sum: requests to the L2 of the 8 XCDs that hit or missed, summed "
+          "over", "the dispatches of one call (dK/dV runs as several dispatches per call).  A miss "
+          "goes on to the", "memory-side Infinity Cache or HBM; the HBM bytes are in the traffic "
+          "summary.", "",
+          "| kernel | dispatches | L2 hits | L2 misses | hit rate |", "|---|---|---|---|---|"]
+    for lab, e in first.items():
+        tot = e["hit"] + e["miss"]
+        rate = e["hit"] / tot if tot else 0.0
+        md.append(f"| {lab} | {e['n']} | {e['hit']:.4e} | {e['miss']:.4e} | {100 * rate:.1f}% |")
+    with open(os.path.join(prof, f"l2_hit_{workload}.md"), "w") as f:
+        f.write("\n".join(md) + "\n")
 
 
 def _summarize_instruction_mix(root, workload, prof, cmd):
@@ -764,8 +805,8 @@ def main():
                          "the GPU)")
     ap.add_argument("--profile-summary", metavar="DIR",
                     help="CPU only: turn the rocprofv3 outputs under DIR (prof_trace, pmc_FETCH_SIZE, "
-                         "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE, pmc_busy; pmc_stall1 and "
-                         "pmc_stall2 when present) into "
+                         "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE, pmc_busy; pmc_l2, pmc_stall1 "
+                         "and pmc_stall2 when present) into "
                          "the summaries under profiles/")
     args = ap.parse_args()
     if args.profile_summary:
