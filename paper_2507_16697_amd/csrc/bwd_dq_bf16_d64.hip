@@ -178,7 +178,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_kernel(
   // The offsets address buffer `cur` of the K and V rings: an exclusive or with kTileBytes at the
   // end of every tile switches them to the other buffer (their lane parts stay below it), so each
   // read is one register plus an immediate.  Opaque, so that the compiler keeps them so.
-  static_assert(32 * C::kRowBytes <= C::kTileBytes, "lane offsets below one tile");
+  static_assert(32 * C::kRowBytes <= C::kTileBytes && (C::kTileBytes & (C::kTileBytes - 1)) == 0,
+                "lane offsets below one tile, whose size is a power of two");
 #pragma unroll
   for (int s = 0; s < C::kDSteps; ++s) asm volatile("" : "+v"(koff[s]));
 #pragma unroll
