@@ -21,6 +21,8 @@ namespace ringx {
 namespace {
 
 constexpr int kTokThreads = 256;
+// four fp32 cells at 4-byte alignment
+typedef float f32x4u __attribute__((ext_vector_type(4), aligned(4)));
 
 __global__ __launch_bounds__(kTokThreads) void tt_tokenize_kernel(
     const float* __restrict__ field, void* __restrict__ tokens, int C, int D, int H, int W, int k,
@@ -93,8 +95,9 @@ __global__ __launch_bounds__(kTokThreads) void tt_tokenize_rows_kernel(
 
   int xs = x0 + pos;
   xs -= xs >= W ? W : 0;
-  // one 16-byte load when the 4 cells neither wrap nor straddle a 16-byte boundary
-  const bool contiguous = active && xs + 4 <= W && (xs & 3) == 0 && (W & 3) == 0;
+  // one 16-byte load when the 4 cells do not wrap (4-byte alignment is all a multi-dword global
+  // load needs, so a subdomain that starts off a 16-byte boundary streams the same way)
+  const bool contiguous = active && xs + 4 <= W;
   const float* fc = field + (int64_t)c * D * H * W;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < K; ++i) {
@@ -110,7 +113,7 @@ __global__ __launch_bounds__(kTokThreads) void tt_tokenize_rows_kernel(
       if (contiguous) {
         // the field is streamed once: non-temporal loads, except for the unfiltered crop (k = 1),
         // whose short row segments are latency-bound
-        const f32x4* vp = reinterpret_cast<const f32x4*>(rowp + xs);
+        const f32x4u* vp = reinterpret_cast<const f32x4u*>(rowp + xs);
         const f32x4 v = K > 1 ? __builtin_nontemporal_load(vp) : *vp;
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wij, v[e], acc[e]);
