@@ -399,14 +399,14 @@ PROFILE_KERNELS = [
     ("bwd_dq_ds_kernel", "bwd_dq_ds_kernel", "bwd_dq_ds", ["bwd_dq_ds.hip", "ringx_device.h"]),
     ("bwd_dq_kernelILi128E", "bwd_dq_kernel<128>", "bwd_dq", ["bwd_dq_bf16.hip", "ringx_device.h"]),
     ("bwd_pre_bf16_kernelILi128E", "bwd_pre_bf16_kernel<128>", "bwd_pre", ["bwd_pre.hip", "ringx_device.h"]),
-    ("merge_vec4_kernelILb1E", "merge_vec4_kernel<bf16 out>", "lse_merge", ["merge.hip", "ringx_device.h"]),
+    ("merge_vec4_kernelILb1ELi1E", "merge_vec4_kernel<bf16 out>", "lse_merge", ["merge.hip", "ringx_device.h"]),
 ]
 
 
 def _profile_kernel(name):
     """rocprofv3 prints some names mangled and some demangled: match either form."""
     demangled = {"ILi128ELi0E": "<128, 0>", "ILi128ELi1E": "<128, 1>", "ILi128ELb0E": "<128, false>",
-                 "ILi128ELb1E": "<128, true>", "ILi128E": "<128>", "ILb1E": "<true>"}
+                 "ILi128ELb1E": "<128, true>", "ILi128E": "<128>", "ILb1E": "<true>", "ILb1ELi1E": "<true, 1>"}
     for frag, label, key, files in PROFILE_KERNELS:
         if frag in name:
             return label, key, files

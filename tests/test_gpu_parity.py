@@ -210,6 +210,29 @@ def test_merge_ignores_minus_inf_partials():
     assert max_abs_err(to_host_f64(el), rl) <= TOL_F32
 
 
+@pytest.mark.parametrize("d", [4, 12, 64, 72, 128])
+@pytest.mark.parametrize("R", [2, 7, 8, 9])
+def test_merge_vector_paths(d, R):
+    """Standalone Eq. (5) merge on every vector path: one or two 4-column quads per thread (two
+    when d is a multiple of 8 and R < 8), fp32 and bf16 outputs, a row count that leaves a ragged
+    last workgroup."""
+    B, H, Nq = 1, 3, 37
+    rng = np.random.default_rng(100 * d + R)
+    po = rng.standard_normal((R, B, H, Nq, d)).astype(np.float32)
+    pl = (3 * rng.standard_normal((R, B, H, Nq))).astype(np.float32)
+    ro, rl = oa.lse_merge(po.astype(np.float64), pl.astype(np.float64))
+    gpo, gpl = torch.from_numpy(po).cuda(), torch.from_numpy(pl).cuda()
+    eo, el = ringx.ringx_lse_merge(gpo, gpl, out_dtype=torch.float32)
+    assert max_abs_err(to_host_f64(eo), ro) <= TOL_F32
+    assert max_abs_err(to_host_f64(el), rl) <= TOL_F32
+    bo, bl = ringx.ringx_lse_merge(gpo, gpl, out_dtype=torch.bfloat16)
+    got = to_host_f64(bo)
+    # rounding to bf16 (nearest even) moves a value by at most half an ulp, 2^-9 of it; the fp32
+    # sum before it may sit on the other side of a rounding boundary: one ulp
+    assert np.all(np.abs(got - ro) <= 2.0 ** -8 * np.abs(ro) + TOL_F32)
+    assert max_abs_err(to_host_f64(bl), rl) <= TOL_F32
+
+
 def test_bf16_forward_independent_of_R():
     """The chunk count changes only the rounding: R = 1 and R = 8 both meet the oracle bar (two
     bf16 outputs may differ by one bf16 ulp from each other, so they are not compared directly)."""
