@@ -1108,32 +1108,38 @@ def main():
         gen.manual_seed(7)
         C_, D_ = 4, 1024
         field = torch.randn((C_, D_, D_, D_), device=dev, generator=gen)
-        modes = []
-        for k_, ratio in ((1, 8), (4, 2), (8, 1)):
-            centre = (D_ // 2, D_ // 3, D_ // 5)
-            tok = ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, stream=stream)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            # the (1, 8x) crop runs for about 14 us, less than the binding takes to enqueue a
-            # call: a spin kernel holds the stream until all calls are queued, so that the
-            # events time the kernels back to back rather than the host's launch rate
-            torch.cuda._sleep(20_000_000)
-            e0.record(stream)
-            for _ in range(20):
-                ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, tokens=tok, stream=stream)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            tms = e0.elapsed_time(e1) / 20
-            nbytes = C_ * (D_ // ratio) ** 3 * 4 + tok.numel() * 4
-            modes.append({"filter": k_, "ratio": ratio, "tokens": tok.shape[0], "ms": tms,
-                          "bytes": nbytes, "GB/s": nbytes / (tms * 1e-3) / 1e9,
-                          "frac": nbytes / (tms * 1e-3) / 1e9 / PEAK_HBM_GBS})
-            del tok
+        def time_modes(centre):
+            modes = []
+            for k_, ratio in ((1, 8), (4, 2), (8, 1)):
+                tok = ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, stream=stream)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                # the (1, 8x) crop runs for about 14 us, less than the binding takes to enqueue a
+                # call: a spin kernel holds the stream until all calls are queued, so that the
+                # events time the kernels back to back rather than the host's launch rate
+                torch.cuda._sleep(20_000_000)
+                e0.record(stream)
+                for _ in range(20):
+                    ringx.ringx_tt_tokenize(field, k_, ratio, centre, 1, tokens=tok, stream=stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                tms = e0.elapsed_time(e1) / 20
+                nbytes = C_ * (D_ // ratio) ** 3 * 4 + tok.numel() * 4
+                modes.append({"filter": k_, "ratio": ratio, "tokens": tok.shape[0], "ms": tms,
+                              "bytes": nbytes, "GB/s": nbytes / (tms * 1e-3) / 1e9,
+                              "frac": nbytes / (tms * 1e-3) / 1e9 / PEAK_HBM_GBS})
+                del tok
+            return modes
+
+        # subdomains starting on a 16-byte boundary along x, and one cell off it (three of four
+        # crop centres)
+        modes = time_modes((D_ // 2, D_ // 3, D_ // 5))
+        modes_off = time_modes((D_ // 2, D_ // 3, D_ // 5 + 1))
         kernels["tt_tokenize"] = {"field": f"{C_}x{D_}^3 fp32", "patch": 1, "modes": modes,
-                                  "bound": "hbm"}
-        log("[bench] tokenizer: " + ", ".join(f"(k={m['filter']}, {m['ratio']}x) "
-                                              f"{m['ms']:.3f} ms {m['GB/s']:.0f} GB/s"
-                                              for m in modes))
+                                  "modes_misaligned": modes_off, "bound": "hbm"}
+        for lab, ms_ in (("aligned", modes), ("misaligned", modes_off)):
+            log(f"[bench] tokenizer, {lab} subdomain: " + ", ".join(
+                f"(k={m['filter']}, {m['ratio']}x) {m['ms']:.3f} ms {m['GB/s']:.0f} GB/s" for m in ms_))
         del field
 
     # the other paper-shaped workloads (parity-test cases, reported beside the headline)
